@@ -1,0 +1,262 @@
+#!/usr/bin/env python3
+"""Benchmark: checksum-protected convolution layers on one MI355X.
+
+Workload: the AlexNet-shaped stack of five convolution layers, fp32, batch 64
+(synthetic U(0,1) inputs and He-normal weights at every layer's own input
+shape; layers are independent).  One step runs the whole protected path of
+every layer on one stream:
+
+    encode(D) -> conv_fwd -> checksum_conv(Co5, Co6, Co7) -> verify -> correct
+
+following the paper's error-injection protocol (Sec. 6.1): step i corrupts one
+output element of layer (i mod 5) between the convolution and the
+verification, so every step also detects, locates and repairs one fault.
+Weight checksums are encoded once at set-up (Sec. 4.2).
+
+Reported: protected TFLOP/s (value), the error-free protected and the
+unprotected (convolution only) rates, ABFT overhead percentages, per-layer
+stage times, a roofline entry for the dominant convolution kernel, and the CPU
+oracle timed on a sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_PEAK_F32 = 157.3   # TFLOP/s, MI355X dense fp32 matrix
+FAULT_VALUE = 100.0     # additive corruption, about 120x the rms of these outputs
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-images", type=int, default=32)
+    ap.add_argument("--quiet", action="store_true")
+    return ap.parse_args()
+
+
+class LayerRun:
+    def __init__(self, cfg, li, ft, torch):
+        import workloads as wl
+        self.spec = spec = cfg.layers[li]
+        self.name = spec.name
+        self.lay = ft.Layer(spec.n, spec.ch, spec.h, spec.w, spec.m, spec.r, spec.s, spec.stride,
+                            spec.pad, spec.dtype)
+        self.D = torch.from_numpy(wl.gen_d(cfg, li)).cuda()
+        self.W = torch.from_numpy(wl.gen_w(cfg, li)).cuda()
+        self.O = self.lay.empty_output()
+        self.lay.encode_weights(self.W)
+        E, F = self.lay.E, self.lay.F
+        self.flops = 2.0 * spec.n * spec.m * E * F * spec.ch * spec.r * spec.s
+        d = wl.fault_draws(cfg.cid, li, 1)[0]
+        self.fault = {"n": int(d[0] * spec.n), "m": int(d[1] * spec.m), "x": int(d[2] * E),
+                      "y": int(d[3] * F), "kind": "add", "value": FAULT_VALUE}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the protected layer needs no communication; see DESIGN.md for how it would shard)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2003_12203_amd as ft
+    import workloads as wl
+
+    ft.lib()  # fails loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    cfg = wl.config(1)
+    runs = [LayerRun(cfg, li, ft, torch) for li in range(len(cfg.layers))]
+    nl = len(runs)
+    total_flops = sum(r.flops for r in runs)
+    torch.cuda.synchronize()
+
+    def protected_step(i, inject=True, ev=None):
+        for li, r in enumerate(runs):
+            L = r.lay
+            L.encode_input(r.D)
+            if ev is not None:
+                ev[li][0].record()
+            L.conv(r.D, r.W, r.O)
+            if ev is not None:
+                ev[li][1].record()
+            L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+            if inject and li == i % nl:
+                L.inject(r.O, [r.fault])
+            L.verify(r.O)
+            L.correct(r.D, r.W, r.O)
+
+    def conv_step(ev=None):
+        for li, r in enumerate(runs):
+            if ev is not None:
+                ev[li][0].record()
+            r.lay.conv(r.D, r.W, r.O)
+            if ev is not None:
+                ev[li][1].record()
+
+    def timed(fn, steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            fn(i)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps
+
+    def mk_events():
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in runs]
+
+    # warm-up (also compiles nothing: kernels are prebuilt)
+    for i in range(args.warmup):
+        protected_step(i)
+        conv_step()
+    torch.cuda.synchronize()
+
+    # ---- the timed region: K protected steps, one injected fault per step -------------
+    step_events = [mk_events() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        protected_step(i, True, step_events[i])
+    torch.cuda.synchronize()
+    t_prot = (time.perf_counter() - t0) / args.steps
+
+    # correctness of the last step: its faulted layer must report one CoC repair at the fault
+    last = runs[(args.steps - 1) % nl]
+    rep = last.lay.read_report()
+    f = last.fault
+    ok_fault = (rep.detected and rep.status == ft.STATUS_CORRECTED
+                and rep.fixes == [(f["n"], f["m"], f["x"], f["y"], ft.SCHEME_COC)])
+    clean_ok = all(not r.lay.read_report().detected for r in runs if r is not last)
+
+    conv_ms = np.array([[step_events[i][li][0].elapsed_time(step_events[i][li][1]) for li in range(nl)]
+                        for i in range(args.steps)])  # [step][layer]
+
+    # ---- reference loops: error-free protected, unprotected --------------------------
+    t_clean = timed(lambda i: protected_step(i, False), args.steps)
+    t_unprot = timed(lambda i: conv_step(), args.steps)
+
+    # ---- per-layer stage breakdown (events between the calls) ------------------------
+    stages = ["encode", "conv", "checksum_conv", "verify", "correct"]
+    reps = max(3, min(args.steps, 10))
+    stage_ms = np.zeros((reps, nl, len(stages)))
+    for k in range(reps):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in runs]
+        for li, r in enumerate(runs):
+            L = r.lay
+            e = evs[li]
+            e[0].record()
+            L.encode_input(r.D)
+            e[1].record()
+            L.conv(r.D, r.W, r.O)
+            e[2].record()
+            L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+            e[3].record()
+            L.verify(r.O)
+            e[4].record()
+            L.correct(r.D, r.W, r.O)
+            e[5].record()
+        torch.cuda.synchronize()
+        for li in range(nl):
+            for s in range(len(stages)):
+                stage_ms[k, li, s] = evs[li][s].elapsed_time(evs[li][s + 1])
+    stage_med = np.median(stage_ms, axis=0)
+
+    per_layer = []
+    for li, r in enumerate(runs):
+        conv_t = float(np.median(conv_ms[:, li]))
+        prot_t = float(stage_med[li].sum())
+        per_layer.append({
+            "layer": r.name, "gflop": round(r.flops / 1e9, 3),
+            "conv_ms": round(conv_t, 4),
+            "conv_tflops": round(r.flops / conv_t / 1e9, 2),
+            "protected_ms": round(prot_t, 4),
+            "protected_tflops": round(r.flops / prot_t / 1e9, 2),
+            "overhead_pct": round((prot_t / float(stage_med[li][1]) - 1) * 100, 2),
+            "stage_ms": {s: round(float(stage_med[li][k]), 4) for k, s in enumerate(stages)},
+        })
+
+    # ---- roofline of the dominant kernel: the 128x128-tile fp32 convolution, which runs
+    # every layer with more than 96 filters (conv2-conv5, 90% of the flops)
+    dom = [li for li, r in enumerate(runs) if r.spec.m > 96]
+    dom_flops = float(np.mean([runs[li].flops for li in dom]))
+    dom_ms = float(np.mean(conv_ms[:, dom]))
+    achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_PEAK_F32, "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_PEAK_F32, 4), "traffic": None,
+                "kernel": "conv_kernel<F32T,2,2,2,2> (conv2-conv5)",
+                "flop_per_launch": dom_flops, "avg_launch_ms": round(dom_ms, 4)}
+
+    # ---- CPU oracle on a bounded sample ----------------------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, args.cpu_sample_images)
+
+    value = total_flops / t_prot / 1e12
+    out = {
+        "metric": "protected conv TFLOP/s per layer + ABFT overhead % vs unprotected conv",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_prot * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "alexnet-5conv-fp32-b64", "batch": 64, "layers": nl,
+                   "faults_per_step": 1, "gflop_per_step": round(total_flops / 1e9, 3)},
+        "error_free_tflops": round(total_flops / t_clean / 1e12, 3),
+        "unprotected_tflops": round(total_flops / t_unprot / 1e12, 3),
+        "overhead_error_free_pct": round((t_clean / t_unprot - 1) * 100, 2),
+        "overhead_erroneous_pct": round((t_prot / t_unprot - 1) * 100, 2),
+        "fault_corrected": bool(ok_fault),
+        "clean_layers_clean": bool(clean_ok),
+        "per_layer": per_layer,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+    return 0 if ok_fault and clean_ok else 1
+
+
+def cpu_baseline(cfg, images):
+    """The oracle's protected layer (encode, direct convolution, checksums, verify, correct), timed on
+    the first `images` images of every layer's batch, with one fault in the third layer."""
+    from oracle import core
+    from oracle import workflow as wf
+    import workloads as wl
+
+    flops = 0.0
+    t0 = time.perf_counter()
+    for li, spec in enumerate(cfg.layers):
+        n = min(images, spec.n)
+        D = wl.gen_d(cfg, li)[:n]
+        W = wl.gen_w(cfg, li)
+        E = core.out_extent(spec.h, spec.r, spec.stride, spec.pad)
+        faults = [wf.Fault(0, 0, E // 2, E // 2, "add", value=FAULT_VALUE)] if li == 2 else []
+        wf.protect(D, W, spec.stride, spec.pad, spec.dtype, faults=faults)
+        flops += 2.0 * n * spec.m * E * E * spec.ch * spec.r * spec.s
+    dt = time.perf_counter() - t0
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": core.num_threads(),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"alexnet 5 conv layers, first {images} of 64 images per layer, one fault in conv3"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

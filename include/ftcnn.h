@@ -1,0 +1,213 @@
+/*
+ * ftcnn.h — checksum-protected convolution on AMD MI355X (gfx950).
+ *
+ * Implements the algorithm-based fault tolerance of FT-CNN (Zhao et al.,
+ * "FT-CNN: Algorithm-Based Fault Tolerance for Convolutional Neural
+ * Networks", arXiv 2003.12203) for one convolution layer:
+ *
+ *   encode    input checksums Cd1, Cd2 of D and Cw1, Cw2 of W     (Sec. 3.2)
+ *   conv_fwd  the layer itself, O = D (x) W                       (Sec. 2.1, eq. 1)
+ *   checksum  output checksums Co1..Co7 as convolutions of        (Sec. 3.2)
+ *   _conv     checksum blocks
+ *   verify    CoC-D detection: So5 = sum_{n,m} O_nm against Co5    (Sec. 3.6, Sec. 4.3)
+ *   correct   the correction chain CoC -> RC -> ClC -> FC          (Sec. 3.3-3.6, 4.1, 4.3)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every tensor pointer is a DEVICE pointer owned by the caller.  The
+ *   library never allocates, frees or retains device memory; scratch comes
+ *   from a caller-supplied workspace of ftcnn_workspace_bytes() bytes
+ *   (256-byte aligned).
+ * - Layouts are dense row-major: D [n][ch][h][w], W [m][ch][r][s],
+ *   O [n][m][E][F] with E = floor((h + 2*pad - r)/stride) + 1 and
+ *   F = floor((w + 2*pad - s)/stride) + 1.  D, W and O share the dtype of the
+ *   descriptor (fp32, or bf16 as raw 16-bit patterns); accumulation is fp32 in
+ *   the convolution and fp64 everywhere on the checksum side.
+ * - Checksum arrays are float64: Cd1, Cd2 [ch][h][w]; Cw1, Cw2 [ch][r][s];
+ *   Co5, Co6, Co7, So5, So6, So7, Q5 [E][F]; Co1, Co3 [m][E][F];
+ *   Co2, Co4 [n][E][F].
+ * - Block index weights: Cd2 = sum_n (n + wbase) D_n, Cw2 = sum_m (m + wbase) W_m,
+ *   and the weighted summations use the same weights.  wbase = 0 is the
+ *   paper's definition (Sec. 3.2).
+ * - Calls taking a stream are asynchronous on it and never synchronize it.
+ *   The shape and size queries are host-only.
+ * - Return value: FTCNN_OK (0) or a negative FTCNN_E_* code; on error the
+ *   stream receives no work and ftcnn_last_error() describes the failure.
+ *   A detected soft error is NOT an error: it is reported in ftcnn_report.
+ * - Functions are thread-safe for distinct streams and distinct buffers.
+ *   Calls sharing a workspace or report must be ordered on one stream.
+ */
+#ifndef FTCNN_H
+#define FTCNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    FTCNN_OK = 0,
+    FTCNN_E_ARG = -1,          /* null pointer or inconsistent argument          */
+    FTCNN_E_SHAPE = -2,        /* non-positive or oversized dimension            */
+    FTCNN_E_DTYPE = -3,        /* dtype not FTCNN_F32 / FTCNN_BF16               */
+    FTCNN_E_WORKSPACE = -4,    /* workspace missing or misaligned                */
+    FTCNN_E_HIP = -5,          /* kernel launch failed                           */
+    FTCNN_E_UNSUPPORTED = -6   /* e.g. groups != 1                               */
+};
+
+typedef enum { FTCNN_F32 = 0, FTCNN_BF16 = 1 } ftcnn_dtype;
+
+/* One convolution layer (notation of Sec. 2.1, Table 1: N, Ch, H, M, R, U). */
+typedef struct {
+    int32_t n, ch, h, w;     /* D [n][ch][h][w]                                  */
+    int32_t m, r, s;         /* W [m][ch][r][s]                                  */
+    int32_t stride, pad;     /* U of eq. (1); zero padding on every side         */
+    int32_t groups;          /* must be 1                                        */
+    int32_t dtype;           /* ftcnn_dtype of D, W and O                        */
+    int32_t wbase;           /* block index weight offset, 0 or 1                */
+} ftcnn_conv_desc;
+
+/* Device pointers to the float64 checksum arrays of one layer (Sec. 3.2).
+ * A call reads or writes only the members its description names; the others
+ * may be NULL.  The struct itself lives in host memory. */
+typedef struct {
+    double *cd1, *cd2;              /* [ch][h][w]   input checksums of D   */
+    double *cw1, *cw2;              /* [ch][r][s]   input checksums of W   */
+    double *co5, *co6, *co7;        /* [E][F]       checksum of checksums  */
+    double *so5, *so6, *so7, *q5;   /* [E][F]       summations of O, and sqrt(sum O^2) */
+    double *co1, *co3;              /* [m][E][F]    row checksums          */
+    double *co2, *co4;              /* [n][E][F]    column checksums       */
+} ftcnn_checksums;
+
+/* Correction schemes, as recorded per repaired element and per position. */
+enum {
+    FTCNN_SCHEME_NONE = 0,
+    FTCNN_SCHEME_COC = 1,          /* checksum-of-checksum, Sec. 3.6          */
+    FTCNN_SCHEME_RC = 2,           /* row checksum, Sec. 3.4                  */
+    FTCNN_SCHEME_CLC = 3,          /* column checksum, Sec. 3.5               */
+    FTCNN_SCHEME_FC = 4,           /* full checksum, Sec. 3.3 and Sec. 4.1.5  */
+    FTCNN_SCHEME_CKSUM = 5,        /* the checksums were corrupt, Sec. 4.1.4  */
+    FTCNN_SCHEME_UNRESOLVED = 6    /* left for recomputation, Sec. 4.1.1      */
+};
+
+enum {
+    FTCNN_STATUS_CLEAN = 0,            /* nothing detected                        */
+    FTCNN_STATUS_CORRECTED = 1,        /* every flagged position resolved         */
+    FTCNN_STATUS_NEEDS_RECOMPUTE = 2,  /* some position unresolved: rerun the layer */
+    FTCNN_STATUS_RECOMPUTED = 3,       /* set by a caller that reran and re-verified */
+    FTCNN_STATUS_FAILED = 4            /* set by a caller whose rerun still mismatches */
+};
+
+typedef struct { int32_t n, m, x, y, scheme; } ftcnn_fix;
+
+/* Detection and correction report, in device (or device-visible host) memory.
+ * ftcnn_verify() resets it; ftcnn_correct() fills in the repairs.  fixes[] is
+ * in no particular order; n_fixes counts every repair even past cap_fixes. */
+typedef struct {
+    int32_t detected;          /* CoC-D verdict for the layer                     */
+    int32_t n_flagged;         /* positions p with Co5 - So5 beyond tolerance     */
+    int32_t status;            /* FTCNN_STATUS_*                                  */
+    int32_t resolved_by[7];    /* positions per FTCNN_SCHEME_*                    */
+    int32_t n_fixes;
+    int32_t cap_fixes;
+    int32_t reserved[2];
+    ftcnn_fix fixes[];
+} ftcnn_report;
+
+/* Tolerance and workflow policy.  A checksum difference d at one element is
+ * bad when it is non-finite or |d| > kappa * (2^-24 sqrt(ch*r*s) + u_out) * Q,
+ * Q being the root sum of squares of the weighted terms of the summation and
+ * u_out = 0 (fp32) or 2^-8 (bf16).  A located index is legal when its ratio is
+ * within eta of an integer inside the index range.  rc_on / clc_on enable the
+ * RC and ClC stages per layer (Sec. 4.3). */
+enum { FTCNN_REPAIR_CHECKSUM = 0, FTCNN_REPAIR_RECOMPUTE = 1 };
+typedef struct {
+    int32_t rc_on, clc_on;
+    int32_t repair;            /* FTCNN_REPAIR_*: exclusive checksum sum, or eq. (1) again */
+    int32_t reserved;
+    double kappa, eta;         /* defaults 16 and 0.1                             */
+} ftcnn_policy;
+
+/* ---- host-only queries -------------------------------------------------- */
+
+/* E and F of eq. (1) with zero padding.  Returns FTCNN_E_SHAPE when either is < 1. */
+int ftcnn_out_shape(const ftcnn_conv_desc *desc, int32_t *E, int32_t *F);
+
+/* Bytes of workspace every call on this layer may use (0 on a bad descriptor). */
+size_t ftcnn_workspace_bytes(const ftcnn_conv_desc *desc);
+
+/* Bytes of an ftcnn_report holding cap_fixes repairs. */
+size_t ftcnn_report_bytes(int32_t cap_fixes);
+
+/* Description of the last error on the calling thread ("" if none). */
+const char *ftcnn_last_error(void);
+
+/* ---- device work -------------------------------------------------------- */
+
+/* Sec. 3.2 input checksums.  which = 0: X is D, c1 = Cd1 = sum_n D_n and
+ * c2 = Cd2 = sum_n (n + wbase) D_n, each [ch][h][w].  which = 1: X is W,
+ * c1 = Cw1, c2 = Cw2, each [ch][r][s] (computed once per layer, before the
+ * application, Sec. 4.2).  float64 accumulation; deterministic. */
+int ftcnn_encode(const ftcnn_conv_desc *desc, int32_t which, const void *X,
+                 double *c1, double *c2, void *workspace, hipStream_t stream);
+
+/* Eq. (1) without bias, with zero padding: O[n][m][x][y] = sum_{k,i,j}
+ * D[n][k][Ux+i-P][Uy+j-P] W[m][k][i][j].  Implicit GEMM on the matrix cores,
+ * fp32 accumulation, O rounded to the layer dtype (nearest even). */
+int ftcnn_conv_fwd(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                   hipStream_t stream);
+
+/* Output checksums of Sec. 3.2, as convolutions of checksum blocks, float64:
+ *   FTCNN_CO1 | FTCNN_CO3: Co1 = Cd1 (x) W, Co3 = Cd2 (x) W   (reads cd1/cd2, W)
+ *   FTCNN_CO2 | FTCNN_CO4: Co2 = D (x) Cw1, Co4 = D (x) Cw2   (reads D, cw1/cw2)
+ *   FTCNN_CO5..7:          Co5 = Cd1 (x) Cw1, Co6 = Cd1 (x) Cw2, Co7 = Cd2 (x) Cw1
+ * CoC-D needs only Co5; the correction chain computes what else it needs at
+ * the flagged positions by itself, so the full Co1..Co4 arrays are optional. */
+enum { FTCNN_CO1 = 1u << 0, FTCNN_CO2 = 1u << 1, FTCNN_CO3 = 1u << 2, FTCNN_CO4 = 1u << 3,
+       FTCNN_CO5 = 1u << 4, FTCNN_CO6 = 1u << 5, FTCNN_CO7 = 1u << 6 };
+int ftcnn_checksum_conv(const ftcnn_conv_desc *desc, uint32_t which, const void *D,
+                        const void *W, const ftcnn_checksums *ck, hipStream_t stream);
+
+/* CoC-D detection (Sec. 3.6, Sec. 4.3).  Reads O and ck->co5; writes
+ * ck->so5, so6, so7, q5 and a per-position flag map into the workspace;
+ * resets *rep (cap_fixes recorded) and sets rep->detected and rep->n_flagged. */
+int ftcnn_verify(const ftcnn_conv_desc *desc, const void *O, const ftcnn_checksums *ck,
+                 const ftcnn_policy *policy, ftcnn_report *rep, int32_t cap_fixes,
+                 void *workspace, hipStream_t stream);
+
+/* Correction module (Sec. 4.3): one device-gated launch that does nothing
+ * unless rep->detected.  Every flagged position runs CoC, then RC and ClC if
+ * enabled, then FC (with the fallbacks of Sec. 4.1.5), each scheme undone
+ * unless Co5..Co7 agree with the re-summed output afterwards.  Repairs O in
+ * place.  Positions where a weighted checksum agrees while Co5 does not are
+ * re-checked against checksums re-encoded from D and W (Sec. 4.1.4).  Reads
+ * D, W, ck->cd1/cd2/cw1/cw2/co5/co6/co7 and the verify flag map in the
+ * workspace.  Leaves status NEEDS_RECOMPUTE if any position is unresolved;
+ * the caller then reruns ftcnn_conv_fwd and ftcnn_verify (Sec. 4.1.1). */
+int ftcnn_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                  const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                  void *workspace, hipStream_t stream);
+
+/* The whole error-free path of one protected layer on one stream:
+ * encode(D) -> conv_fwd -> checksum_conv(CO5|CO6|CO7) -> verify -> correct.
+ * ck->cw1/cw2 must hold the encoded W (ftcnn_encode with which = 1). */
+int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                         const ftcnn_checksums *ck, const ftcnn_policy *policy,
+                         ftcnn_report *rep, int32_t cap_fixes, void *workspace,
+                         hipStream_t stream);
+
+/* TEST ONLY: corrupt stored outputs, reproducing the paper's source-level
+ * fault injection (Sec. 6.1).  faults is a HOST array of at most 64 entries:
+ * kind 0 flips bit `bit` of the stored pattern, kind 1 adds `value`, kind 2
+ * stores `value` (all rounded to the dtype).  Positions must be in range. */
+typedef struct { int32_t n, m, x, y, kind, bit; double value; } ftcnn_fault;
+int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults, int32_t nf,
+                 hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FTCNN_H */

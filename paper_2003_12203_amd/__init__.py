@@ -1,0 +1,250 @@
+"""Checksum-protected convolution (FT-CNN, arXiv 2003.12203) on MI355X.
+
+A thin Python binding over the C ABI of ``include/ftcnn.h``: the functions
+below have the names of the C entry points and only marshal arguments (torch
+device tensors become raw device pointers, the current torch stream becomes
+the HIP stream).  Every step of the protected layer runs in the library's HIP
+kernels; if ``libftcnn.so`` is missing, every call raises.
+
+``Layer`` bundles the per-layer device buffers (checksums, workspace, report)
+for convenience.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+from typing import Dict, List, Optional, Sequence
+
+import torch
+
+from . import _lib
+from ._lib import (BF16, CO1, CO2, CO3, CO4, CO5, CO6, CO7, F32, REPAIR_CHECKSUM,  # noqa: F401
+                   REPAIR_RECOMPUTE, SCHEME_CKSUM, SCHEME_CLC, SCHEME_COC, SCHEME_FC, SCHEME_NONE,
+                   SCHEME_RC, SCHEME_UNRESOLVED, STATUS_CLEAN, STATUS_CORRECTED, STATUS_FAILED,
+                   STATUS_NEEDS_RECOMPUTE, STATUS_RECOMPUTED)
+
+DTYPES = {"f32": (F32, torch.float32), "bf16": (BF16, torch.bfloat16)}
+
+
+class FtcnnError(RuntimeError):
+    pass
+
+
+def lib():
+    return _lib.load()
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != 0:
+        msg = lib().ftcnn_last_error().decode(errors="replace")
+        raise FtcnnError(f"{what} failed ({rc}): {msg}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise FtcnnError("expected a device tensor")
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def make_desc(n, ch, h, w, m, r, s, stride=1, pad=0, dtype="f32", wbase=0, groups=1) -> _lib.ConvDesc:
+    return _lib.ConvDesc(n, ch, h, w, m, r, s, stride, pad, groups, DTYPES[dtype][0], wbase)
+
+
+def make_policy(rc_on=True, clc_on=True, repair="checksum", kappa=16.0, eta=0.1) -> _lib.Policy:
+    rep = REPAIR_RECOMPUTE if repair == "recompute" else REPAIR_CHECKSUM
+    return _lib.Policy(int(rc_on), int(clc_on), rep, 0, float(kappa), float(eta))
+
+
+# ---- the C entry points --------------------------------------------------------
+
+def out_shape(desc) -> tuple:
+    E, F = C.c_int32(), C.c_int32()
+    _check(lib().ftcnn_out_shape(C.byref(desc), C.byref(E), C.byref(F)), "ftcnn_out_shape")
+    return E.value, F.value
+
+
+def workspace_bytes(desc) -> int:
+    return int(lib().ftcnn_workspace_bytes(C.byref(desc)))
+
+
+def report_bytes(cap: int) -> int:
+    return int(lib().ftcnn_report_bytes(cap))
+
+
+def last_error() -> str:
+    return lib().ftcnn_last_error().decode(errors="replace")
+
+
+def encode(desc, which: int, X: torch.Tensor, c1: torch.Tensor, c2: torch.Tensor,
+           workspace: torch.Tensor, stream=None) -> None:
+    _check(lib().ftcnn_encode(C.byref(desc), which, _ptr(X), _ptr(c1), _ptr(c2), _ptr(workspace),
+                              _stream(stream)), "ftcnn_encode")
+
+
+def conv_fwd(desc, D: torch.Tensor, W: torch.Tensor, O: torch.Tensor, stream=None) -> None:
+    _check(lib().ftcnn_conv_fwd(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), _stream(stream)), "ftcnn_conv_fwd")
+
+
+def checksum_conv(desc, which: int, D, W, ck: _lib.Checksums, stream=None) -> None:
+    _check(lib().ftcnn_checksum_conv(C.byref(desc), which, _ptr(D), _ptr(W), C.byref(ck), _stream(stream)),
+           "ftcnn_checksum_conv")
+
+
+def verify(desc, O, ck, policy, report: torch.Tensor, cap: int, workspace, stream=None) -> None:
+    _check(lib().ftcnn_verify(C.byref(desc), _ptr(O), C.byref(ck), C.byref(policy), _ptr(report), cap,
+                              _ptr(workspace), _stream(stream)), "ftcnn_verify")
+
+
+def correct(desc, D, W, O, ck, policy, report, workspace, stream=None) -> None:
+    _check(lib().ftcnn_correct(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck), C.byref(policy),
+                               _ptr(report), _ptr(workspace), _stream(stream)), "ftcnn_correct")
+
+
+def protected_conv(desc, D, W, O, ck, policy, report, cap, workspace, stream=None) -> None:
+    _check(lib().ftcnn_protected_conv(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck),
+                                      C.byref(policy), _ptr(report), cap, _ptr(workspace),
+                                      _stream(stream)), "ftcnn_protected_conv")
+
+
+def inject(desc, O, faults: Sequence[dict], stream=None) -> None:
+    arr = (_lib.Fault * max(1, len(faults)))()
+    kinds = {"flip": 0, "add": 1, "set": 2}
+    for i, f in enumerate(faults):
+        arr[i] = _lib.Fault(f["n"], f["m"], f["x"], f["y"], kinds[f["kind"]], f.get("bit", 0),
+                            float(f.get("value", 0.0)))
+    _check(lib().ftcnn_inject(C.byref(desc), _ptr(O), arr, len(faults), _stream(stream)), "ftcnn_inject")
+
+
+# ---- report ----------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Report:
+    detected: bool
+    n_flagged: int
+    status: int
+    resolved_by: List[int]
+    fixes: List[tuple]        # sorted (n, m, x, y, scheme)
+    n_fixes: int
+    cap_fixes: int
+
+
+def parse_report(buf: torch.Tensor) -> Report:
+    raw = bytes(buf.cpu().numpy().tobytes())
+    h = _lib.ReportHeader.from_buffer_copy(raw[:C.sizeof(_lib.ReportHeader)])
+    nf = min(h.n_fixes, h.cap_fixes)
+    fixes = []
+    base = C.sizeof(_lib.ReportHeader)
+    for i in range(nf):
+        fx = _lib.Fix.from_buffer_copy(raw[base + i * C.sizeof(_lib.Fix): base + (i + 1) * C.sizeof(_lib.Fix)])
+        fixes.append((fx.n, fx.m, fx.x, fx.y, fx.scheme))
+    fixes.sort()
+    return Report(bool(h.detected), h.n_flagged, h.status, list(h.resolved_by), fixes, h.n_fixes, h.cap_fixes)
+
+
+# ---- per-layer buffers --------------------------------------------------------------
+
+class Layer:
+    """Device buffers of one protected layer and the calls that use them."""
+
+    def __init__(self, n, ch, h, w, m, r, s, stride=1, pad=0, dtype="f32", wbase=0,
+                 policy: Optional[_lib.Policy] = None, cap_fixes: int = 4096, device="cuda"):
+        self.desc = make_desc(n, ch, h, w, m, r, s, stride, pad, dtype, wbase)
+        self.dtype = dtype
+        self.tdtype = DTYPES[dtype][1]
+        self.E, self.F = out_shape(self.desc)
+        self.shape_d = (n, ch, h, w)
+        self.shape_w = (m, ch, r, s)
+        self.shape_o = (n, m, self.E, self.F)
+        self.policy = policy or make_policy()
+        self.cap = cap_fixes
+        dev = torch.device(device)
+        f64 = dict(dtype=torch.float64, device=dev)
+        EF = self.E * self.F
+        self.buf: Dict[str, torch.Tensor] = {
+            "cd1": torch.zeros(ch * h * w, **f64), "cd2": torch.zeros(ch * h * w, **f64),
+            "cw1": torch.zeros(ch * r * s, **f64), "cw2": torch.zeros(ch * r * s, **f64),
+        }
+        for k in ("co5", "co6", "co7", "so5", "so6", "so7", "q5"):
+            self.buf[k] = torch.zeros(EF, **f64)
+        self.ck = _lib.Checksums()
+        self._sync_ck()
+        nbytes = workspace_bytes(self.desc)
+        self._ws_raw = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
+        off = (-self._ws_raw.data_ptr()) % 256
+        self.workspace = self._ws_raw[off:off + nbytes]
+        self.report = torch.zeros(report_bytes(cap_fixes), dtype=torch.uint8, device=dev)
+
+    def _sync_ck(self):
+        for k, t in self.buf.items():
+            setattr(self.ck, k, t.data_ptr())
+
+    def want_row_col(self, rows: bool = True, cols: bool = True):
+        n, m = self.shape_d[0], self.shape_w[0]
+        EF = self.E * self.F
+        dev = self.buf["cd1"].device
+        if rows and "co1" not in self.buf:
+            self.buf["co1"] = torch.zeros(m * EF, dtype=torch.float64, device=dev)
+            self.buf["co3"] = torch.zeros(m * EF, dtype=torch.float64, device=dev)
+        if cols and "co2" not in self.buf:
+            self.buf["co2"] = torch.zeros(n * EF, dtype=torch.float64, device=dev)
+            self.buf["co4"] = torch.zeros(n * EF, dtype=torch.float64, device=dev)
+        self._sync_ck()
+
+    def empty_output(self) -> torch.Tensor:
+        return torch.empty(self.shape_o, dtype=self.tdtype, device=self.buf["cd1"].device)
+
+    # the entry points on this layer's buffers
+    def encode_weights(self, W, stream=None):
+        encode(self.desc, 1, W, self.buf["cw1"], self.buf["cw2"], self.workspace, stream)
+
+    def encode_input(self, D, stream=None):
+        encode(self.desc, 0, D, self.buf["cd1"], self.buf["cd2"], self.workspace, stream)
+
+    def conv(self, D, W, O, stream=None):
+        conv_fwd(self.desc, D, W, O, stream)
+
+    def checksum_conv(self, which, D=None, W=None, stream=None):
+        checksum_conv(self.desc, which, D, W, self.ck, stream)
+
+    def verify(self, O, stream=None):
+        verify(self.desc, O, self.ck, self.policy, self.report, self.cap, self.workspace, stream)
+
+    def correct(self, D, W, O, stream=None):
+        correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.workspace, stream)
+
+    def protected(self, D, W, O, stream=None):
+        protected_conv(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace,
+                       stream)
+
+    def inject(self, O, faults, stream=None):
+        inject(self.desc, O, faults, stream)
+
+    def read_report(self) -> Report:
+        torch.cuda.synchronize()
+        return parse_report(self.report)
+
+    def run(self, D, W, O, faults=(), stream=None) -> Report:
+        """The full workflow of Sec. 4.3 with recomputation of the layer when needed (Sec. 4.1.1)."""
+        self.encode_input(D, stream)
+        self.conv(D, W, O, stream)
+        self.checksum_conv(CO5 | CO6 | CO7, stream=stream)
+        if faults:
+            self.inject(O, faults, stream)
+        self.verify(O, stream)
+        self.correct(D, W, O, stream)
+        rep = self.read_report()
+        if rep.status == STATUS_NEEDS_RECOMPUTE:
+            first = rep
+            self.conv(D, W, O, stream)
+            self.verify(O, stream)
+            again = self.read_report()
+            first.status = STATUS_FAILED if again.detected else STATUS_RECOMPUTED
+            rep = first
+        return rep

@@ -1,0 +1,97 @@
+"""ctypes declarations of the C ABI in include/ftcnn.h (argument marshalling only)."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libftcnn.so")
+
+F32, BF16 = 0, 1
+
+CO1, CO2, CO3, CO4, CO5, CO6, CO7 = (1 << i for i in range(7))
+
+SCHEME_NONE, SCHEME_COC, SCHEME_RC, SCHEME_CLC, SCHEME_FC, SCHEME_CKSUM, SCHEME_UNRESOLVED = range(7)
+STATUS_CLEAN, STATUS_CORRECTED, STATUS_NEEDS_RECOMPUTE, STATUS_RECOMPUTED, STATUS_FAILED = range(5)
+REPAIR_CHECKSUM, REPAIR_RECOMPUTE = 0, 1
+
+
+class ConvDesc(C.Structure):
+    _fields_ = [("n", C.c_int32), ("ch", C.c_int32), ("h", C.c_int32), ("w", C.c_int32),
+                ("m", C.c_int32), ("r", C.c_int32), ("s", C.c_int32),
+                ("stride", C.c_int32), ("pad", C.c_int32), ("groups", C.c_int32),
+                ("dtype", C.c_int32), ("wbase", C.c_int32)]
+
+
+_dp = C.c_void_p
+
+
+class Checksums(C.Structure):
+    _fields_ = [(name, _dp) for name in
+                ("cd1", "cd2", "cw1", "cw2", "co5", "co6", "co7", "so5", "so6", "so7", "q5",
+                 "co1", "co3", "co2", "co4")]
+
+
+class Fix(C.Structure):
+    _fields_ = [("n", C.c_int32), ("m", C.c_int32), ("x", C.c_int32), ("y", C.c_int32),
+                ("scheme", C.c_int32)]
+
+
+class ReportHeader(C.Structure):
+    _fields_ = [("detected", C.c_int32), ("n_flagged", C.c_int32), ("status", C.c_int32),
+                ("resolved_by", C.c_int32 * 7), ("n_fixes", C.c_int32), ("cap_fixes", C.c_int32),
+                ("reserved", C.c_int32 * 2)]
+
+
+class Policy(C.Structure):
+    _fields_ = [("rc_on", C.c_int32), ("clc_on", C.c_int32), ("repair", C.c_int32),
+                ("reserved", C.c_int32), ("kappa", C.c_double), ("eta", C.c_double)]
+
+
+class Fault(C.Structure):
+    _fields_ = [("n", C.c_int32), ("m", C.c_int32), ("x", C.c_int32), ("y", C.c_int32),
+                ("kind", C.c_int32), ("bit", C.c_int32), ("value", C.c_double)]
+
+
+EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ftcnn_last_error",
+           "ftcnn_encode", "ftcnn_conv_fwd", "ftcnn_checksum_conv", "ftcnn_verify", "ftcnn_correct",
+           "ftcnn_protected_conv", "ftcnn_inject")
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2003_12203_amd/build.py "
+                           "(hipcc, gfx950); there is no fallback implementation")
+    L = C.CDLL(path)
+    P = C.POINTER
+    L.ftcnn_out_shape.argtypes = [P(ConvDesc), P(C.c_int32), P(C.c_int32)]
+    L.ftcnn_out_shape.restype = C.c_int
+    L.ftcnn_workspace_bytes.argtypes = [P(ConvDesc)]
+    L.ftcnn_workspace_bytes.restype = C.c_size_t
+    L.ftcnn_report_bytes.argtypes = [C.c_int32]
+    L.ftcnn_report_bytes.restype = C.c_size_t
+    L.ftcnn_last_error.argtypes = []
+    L.ftcnn_last_error.restype = C.c_char_p
+    L.ftcnn_encode.argtypes = [P(ConvDesc), C.c_int32, _dp, _dp, _dp, _dp, _dp]
+    L.ftcnn_encode.restype = C.c_int
+    L.ftcnn_conv_fwd.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp]
+    L.ftcnn_conv_fwd.restype = C.c_int
+    L.ftcnn_checksum_conv.argtypes = [P(ConvDesc), C.c_uint32, _dp, _dp, P(Checksums), _dp]
+    L.ftcnn_checksum_conv.restype = C.c_int
+    L.ftcnn_verify.argtypes = [P(ConvDesc), _dp, P(Checksums), P(Policy), _dp, C.c_int32, _dp, _dp]
+    L.ftcnn_verify.restype = C.c_int
+    L.ftcnn_correct.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp, _dp, _dp]
+    L.ftcnn_correct.restype = C.c_int
+    L.ftcnn_protected_conv.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp,
+                                       C.c_int32, _dp, _dp]
+    L.ftcnn_protected_conv.restype = C.c_int
+    L.ftcnn_inject.argtypes = [P(ConvDesc), _dp, P(Fault), C.c_int32, _dp]
+    L.ftcnn_inject.restype = C.c_int
+    _lib = L
+    return L

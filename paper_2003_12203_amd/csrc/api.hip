@@ -1,0 +1,282 @@
+// The C ABI of include/ftcnn.h: argument checks, the per-layer launch plan and
+// the workspace layout.  All device work is enqueued by the launch_* functions.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "ftcnn_internal.h"
+
+namespace ftcnn {
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *where) {
+    return fail(FTCNN_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
+
+int clampi(long long v, long long lo, long long hi) { return (int)(v < lo ? lo : (v > hi ? hi : v)); }
+
+// Row splits for a column reduction of [rows][cols]: enough workgroups to fill
+// the chip, but every split keeps at least `min_rows` rows.
+int row_splits(long long rows, long long col_blocks, long long target_blocks, long long min_rows) {
+    const long long want = ceil_div(target_blocks, col_blocks);
+    const long long cap = rows / min_rows > 1 ? rows / min_rows : 1;
+    return clampi(want, 1, cap);
+}
+
+int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
+    if (!d) return fail(FTCNN_E_ARG, "null descriptor");
+    if (d->groups != 1) return fail(FTCNN_E_UNSUPPORTED, "groups = %d (only 1 is supported)", d->groups);
+    if (d->dtype != FTCNN_F32 && d->dtype != FTCNN_BF16) return fail(FTCNN_E_DTYPE, "dtype %d", d->dtype);
+    if (d->wbase != 0 && d->wbase != 1) return fail(FTCNN_E_ARG, "wbase %d (0 or 1)", d->wbase);
+    if (d->n < 1 || d->ch < 1 || d->h < 1 || d->w < 1 || d->m < 1 || d->r < 1 || d->s < 1 ||
+        d->stride < 1 || d->pad < 0)
+        return fail(FTCNN_E_SHAPE, "non-positive dimension");
+    Geom &g = pl->g;
+    g.N = d->n; g.C = d->ch; g.H = d->h; g.W = d->w;
+    g.M = d->m; g.R = d->r; g.S = d->s; g.U = d->stride; g.P = d->pad;
+    const long long hs = (long long)d->h + 2LL * d->pad - d->r, ws = (long long)d->w + 2LL * d->pad - d->s;
+    if (hs < 0 || ws < 0) return fail(FTCNN_E_SHAPE, "kernel larger than the padded input");
+    g.E = (int)(hs / d->stride + 1);
+    g.F = (int)(ws / d->stride + 1);
+    const long long K = (long long)d->ch * d->r * d->s;
+    const long long EF = (long long)g.E * g.F;
+    const long long CHW = (long long)d->ch * d->h * d->w;
+    if (K > (1LL << 30) || EF > (1LL << 30) || CHW > (1LL << 30) || d->m > (1 << 20) || d->n > (1 << 20))
+        return fail(FTCNN_E_SHAPE, "dimension beyond the supported range");
+    g.K = (int)K;
+    g.EF = (int)EF;
+    g.CHW = CHW;
+    g.P_total = (long long)g.N * EF;
+    g.dtype = d->dtype;
+    g.wbase = d->wbase;
+
+    const int vec = g.dtype == FTCNN_F32 ? 4 : 8;
+    // input checksums
+    pl->enc_splits_d = row_splits(g.N, ceil_div(ceil_div(CHW, vec), kThreads), 1024, 4);
+    pl->enc_splits_w = row_splits(g.M, ceil_div(ceil_div(K, vec), kThreads), 1024, 4);
+    // verification
+    const long long cols_v = ceil_div(EF, EF % vec == 0 ? vec : 1);
+    const long long ctt = cols_v < kThreads ? cols_v : kThreads;
+    pl->ver_cols_per_block = (int)ctt;
+    pl->ver_splits = row_splits((long long)g.N * g.M, ceil_div(cols_v, ctt), 768, 128);
+    // correction
+    pl->corr_blocks = 256;
+    const long long L = g.M > g.N ? g.M : g.N;
+    pl->corr_stride = (size_t)((4LL * g.M + 4LL * g.N + 2 * L + 31) / 32 * 32);
+
+    size_t off = 0;
+    pl->off_flags = off;
+    off += align256(sizeof(int) * (size_t)EF);
+    pl->off_enc = off;
+    const size_t enc_d = pl->enc_splits_d > 1 ? 2ull * pl->enc_splits_d * CHW * sizeof(double) : 0;
+    const size_t enc_w = pl->enc_splits_w > 1 ? 2ull * pl->enc_splits_w * K * sizeof(double) : 0;
+    off += align256(enc_d > enc_w ? enc_d : enc_w);
+    pl->off_ver = off;
+    off += align256(4ull * pl->ver_splits * EF * sizeof(double));
+    pl->off_corr = off;
+    off += align256((size_t)pl->corr_blocks * pl->corr_stride * sizeof(double));
+    pl->bytes = off;
+    return FTCNN_OK;
+}
+
+int check_ws(const Plan &pl, const void *ws) {
+    if (!ws) return fail(FTCNN_E_WORKSPACE, "null workspace (%zu bytes needed)", pl.bytes);
+    if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(FTCNN_E_WORKSPACE, "workspace not 256-byte aligned");
+    return FTCNN_OK;
+}
+
+#define FT_TRY(expr)                  \
+    do {                              \
+        const int _rc = (expr);       \
+        if (_rc != FTCNN_OK) return _rc; \
+    } while (0)
+
+#define FT_HIP(expr, where)                          \
+    do {                                             \
+        const hipError_t _e = (expr);                \
+        if (_e != hipSuccess) return hip_fail(_e, where); \
+    } while (0)
+
+int check_policy(const ftcnn_policy *p) {
+    if (!p) return fail(FTCNN_E_ARG, "null policy");
+    if (!(p->kappa > 0.0) || !(p->eta >= 0.0 && p->eta < 0.5))
+        return fail(FTCNN_E_ARG, "policy needs kappa > 0 and 0 <= eta < 0.5");
+    if (p->repair != FTCNN_REPAIR_CHECKSUM && p->repair != FTCNN_REPAIR_RECOMPUTE)
+        return fail(FTCNN_E_ARG, "policy repair %d", p->repair);
+    return FTCNN_OK;
+}
+
+int do_encode(const Plan &pl, int which, const void *X, double *c1, double *c2, void *ws, hipStream_t st) {
+    if (which != 0 && which != 1) return fail(FTCNN_E_ARG, "encode which = %d (0 = D, 1 = W)", which);
+    if (!X || !c1 || !c2) return fail(FTCNN_E_ARG, "encode: null pointer");
+    const int splits = which == 0 ? pl.enc_splits_d : pl.enc_splits_w;
+    if (splits > 1) FT_TRY(check_ws(pl, ws));
+    FT_HIP(launch_encode(pl, which, X, c1, c2, ws, st), "encode");
+    return FTCNN_OK;
+}
+
+int do_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st) {
+    if (!D || !W || !O) return fail(FTCNN_E_ARG, "conv_fwd: null pointer");
+    FT_HIP(launch_conv(pl, D, W, O, st), "conv_fwd");
+    return FTCNN_OK;
+}
+
+int do_cksum(const Plan &pl, uint32_t which, const void *D, const void *W, const ftcnn_checksums *ck,
+             hipStream_t st) {
+    if (!ck) return fail(FTCNN_E_ARG, "checksum_conv: null checksums");
+    if (which & ~0x7Fu) return fail(FTCNN_E_ARG, "checksum_conv: unknown bits 0x%x", which);
+    if ((which & (FTCNN_CO5 | FTCNN_CO6)) && !ck->cd1) return fail(FTCNN_E_ARG, "Co5/Co6 need cd1");
+    if ((which & (FTCNN_CO5 | FTCNN_CO7)) && !ck->cw1) return fail(FTCNN_E_ARG, "Co5/Co7 need cw1");
+    if ((which & FTCNN_CO6) && !ck->cw2) return fail(FTCNN_E_ARG, "Co6 needs cw2");
+    if ((which & FTCNN_CO7) && !ck->cd2) return fail(FTCNN_E_ARG, "Co7 needs cd2");
+    if ((which & FTCNN_CO7) && !(which & FTCNN_CO5) && !ck->cd1) return fail(FTCNN_E_ARG, "Co7 needs cd1");
+    if ((which & FTCNN_CO5) && !ck->co5) return fail(FTCNN_E_ARG, "null co5");
+    if ((which & FTCNN_CO6) && !ck->co6) return fail(FTCNN_E_ARG, "null co6");
+    if ((which & FTCNN_CO7) && !ck->co7) return fail(FTCNN_E_ARG, "null co7");
+    if ((which & (FTCNN_CO1 | FTCNN_CO3)) && (!W || !ck->cd1 || !ck->cd2))
+        return fail(FTCNN_E_ARG, "Co1/Co3 need W, cd1 and cd2");
+    if ((which & (FTCNN_CO2 | FTCNN_CO4)) && (!D || !ck->cw1 || !ck->cw2))
+        return fail(FTCNN_E_ARG, "Co2/Co4 need D, cw1 and cw2");
+    if (((which & FTCNN_CO1) && !ck->co1) || ((which & FTCNN_CO3) && !ck->co3) ||
+        ((which & FTCNN_CO2) && !ck->co2) || ((which & FTCNN_CO4) && !ck->co4))
+        return fail(FTCNN_E_ARG, "checksum_conv: null output array");
+    FT_HIP(launch_checksum_conv(pl, which, D, W, *ck, st), "checksum_conv");
+    return FTCNN_OK;
+}
+
+int do_verify(const Plan &pl, const void *O, const ftcnn_checksums *ck, const ftcnn_policy *pol,
+              ftcnn_report *rep, int32_t cap, void *ws, hipStream_t st) {
+    FT_TRY(check_policy(pol));
+    if (!O || !ck || !rep) return fail(FTCNN_E_ARG, "verify: null pointer");
+    if (!ck->co5 || !ck->so5 || !ck->so6 || !ck->so7 || !ck->q5)
+        return fail(FTCNN_E_ARG, "verify needs co5, so5, so6, so7 and q5");
+    if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
+    FT_TRY(check_ws(pl, ws));
+    FT_HIP(launch_verify(pl, O, *ck, *pol, rep, cap, ws, st), "verify");
+    return FTCNN_OK;
+}
+
+int do_correct(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
+               const ftcnn_policy *pol, ftcnn_report *rep, void *ws, hipStream_t st) {
+    FT_TRY(check_policy(pol));
+    if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "correct: null pointer");
+    if (!ck->cd1 || !ck->cd2 || !ck->cw1 || !ck->cw2 || !ck->co5 || !ck->co6 || !ck->co7)
+        return fail(FTCNN_E_ARG, "correct needs cd1, cd2, cw1, cw2, co5, co6 and co7");
+    FT_TRY(check_ws(pl, ws));
+    FT_HIP(launch_correct(pl, D, W, O, *ck, *pol, rep, ws, st), "correct");
+    return FTCNN_OK;
+}
+
+}  // namespace
+}  // namespace ftcnn
+
+using namespace ftcnn;
+
+extern "C" {
+
+const char *ftcnn_last_error(void) { return g_err; }
+
+int ftcnn_out_shape(const ftcnn_conv_desc *desc, int32_t *E, int32_t *F) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (E) *E = pl.g.E;
+    if (F) *F = pl.g.F;
+    return FTCNN_OK;
+}
+
+size_t ftcnn_workspace_bytes(const ftcnn_conv_desc *desc) {
+    Plan pl;
+    if (make_plan(desc, &pl) != FTCNN_OK) return 0;
+    return pl.bytes;
+}
+
+size_t ftcnn_report_bytes(int32_t cap_fixes) {
+    return sizeof(ftcnn_report) + (size_t)(cap_fixes > 0 ? cap_fixes : 0) * sizeof(ftcnn_fix);
+}
+
+int ftcnn_encode(const ftcnn_conv_desc *desc, int32_t which, const void *X, double *c1, double *c2,
+                 void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_encode(pl, which, X, c1, c2, workspace, stream);
+}
+
+int ftcnn_conv_fwd(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_conv(pl, D, W, O, stream);
+}
+
+int ftcnn_checksum_conv(const ftcnn_conv_desc *desc, uint32_t which, const void *D, const void *W,
+                        const ftcnn_checksums *ck, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_cksum(pl, which, D, W, ck, stream);
+}
+
+int ftcnn_verify(const ftcnn_conv_desc *desc, const void *O, const ftcnn_checksums *ck,
+                 const ftcnn_policy *policy, ftcnn_report *rep, int32_t cap_fixes, void *workspace,
+                 hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_verify(pl, O, ck, policy, rep, cap_fixes, workspace, stream);
+}
+
+int ftcnn_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                  const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                  void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_correct(pl, D, W, O, ck, policy, rep, workspace, stream);
+}
+
+int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                         const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                         int32_t cap_fixes, void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    FT_TRY(check_policy(policy));
+    if (!ck || !D || !W || !O || !rep) return fail(FTCNN_E_ARG, "protected_conv: null pointer");
+    FT_TRY(check_ws(pl, workspace));
+    FT_TRY(do_encode(pl, 0, D, ck->cd1, ck->cd2, workspace, stream));
+    FT_TRY(do_conv(pl, D, W, O, stream));
+    FT_TRY(do_cksum(pl, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, D, W, ck, stream));
+    FT_TRY(do_verify(pl, O, ck, policy, rep, cap_fixes, workspace, stream));
+    return do_correct(pl, D, W, O, ck, policy, rep, workspace, stream);
+}
+
+int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults, int32_t nf,
+                 hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (!O || (nf > 0 && !faults)) return fail(FTCNN_E_ARG, "inject: null pointer");
+    if (nf < 0 || nf > kMaxFaults) return fail(FTCNN_E_ARG, "inject: %d faults (at most %d)", nf, kMaxFaults);
+    const Geom &g = pl.g;
+    const int bits = g.dtype == FTCNN_F32 ? 32 : 16;
+    for (int i = 0; i < nf; ++i) {
+        const ftcnn_fault &f = faults[i];
+        if (f.n < 0 || f.n >= g.N || f.m < 0 || f.m >= g.M || f.x < 0 || f.x >= g.E || f.y < 0 || f.y >= g.F)
+            return fail(FTCNN_E_ARG, "inject: fault %d out of range", i);
+        if (f.kind < 0 || f.kind > 2 || (f.kind == 0 && (f.bit < 0 || f.bit >= bits)))
+            return fail(FTCNN_E_ARG, "inject: fault %d has kind %d bit %d", i, f.kind, f.bit);
+    }
+    if (nf == 0) return FTCNN_OK;
+    FT_HIP(launch_inject(pl, O, faults, nf, stream), "inject");
+    return FTCNN_OK;
+}
+
+}  // extern "C"

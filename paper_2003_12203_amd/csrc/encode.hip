@@ -1,0 +1,146 @@
+// Input checksums (Sec. 3.2): C1 = sum_r X_r and C2 = sum_r (r + wbase) X_r over
+// the leading block index of X [rows][cols] (D over images, W over filters).
+//
+// A streaming column reduction: consecutive lanes own consecutive columns, so
+// every row is read with full-width coalesced 16-byte loads, and each lane keeps
+// its running sums in float64 registers.  Rows are split across a second grid
+// dimension when there are too few columns to fill the chip; the split partials
+// are combined in a fixed order, so the result is deterministic.
+#include "ftcnn_internal.h"
+
+namespace ftcnn {
+namespace {
+
+template <typename T, int VEC> struct Vec;
+template <> struct Vec<float, 1> {
+    __device__ static void load(const float *p, float (&v)[1]) { v[0] = *p; }
+};
+template <> struct Vec<float, 4> {
+    __device__ static void load(const float *p, float (&v)[4]) {
+        const float4 q = *reinterpret_cast<const float4 *>(p);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    }
+};
+template <> struct Vec<uint16_t, 1> {
+    __device__ static void load(const uint16_t *p, float (&v)[1]) { v[0] = bf16_bits_to_f32(*p); }
+};
+template <> struct Vec<uint16_t, 8> {
+    __device__ static void load(const uint16_t *p, float (&v)[8]) {
+        const uint4 q = *reinterpret_cast<const uint4 *>(p);
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = __builtin_bit_cast(float, w[i] << 16);
+            v[2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xFFFF0000u);
+        }
+    }
+};
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(kThreads) void encode_partial(const T *__restrict__ X, long long rows,
+                                                           long long cols, int wbase,
+                                                           double *__restrict__ c1,
+                                                           double *__restrict__ c2,
+                                                           double *__restrict__ part) {
+    const long long col = ((long long)blockIdx.x * kThreads + threadIdx.x) * VEC;
+    if (col >= cols) return;
+    const int splits = gridDim.y;
+    const long long rps = (rows + splits - 1) / splits;
+    const long long r0 = (long long)blockIdx.y * rps;
+    const long long r1 = r0 + rps < rows ? r0 + rps : rows;
+
+    double s1[VEC], s2[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) s1[v] = s2[v] = 0.0;
+
+    long long r = r0;
+    for (; r + 4 <= r1; r += 4) {
+        float x[4][VEC];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) Vec<T, VEC>::load(X + (r + u) * cols + col, x[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const double wgt = (double)(r + u + wbase);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                const double e = (double)x[u][v];
+                s1[v] += e;
+                s2[v] = fma(wgt, e, s2[v]);
+            }
+        }
+    }
+    for (; r < r1; ++r) {
+        float x[VEC];
+        Vec<T, VEC>::load(X + r * cols + col, x);
+        const double wgt = (double)(r + wbase);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            s1[v] += (double)x[v];
+            s2[v] = fma(wgt, (double)x[v], s2[v]);
+        }
+    }
+    if (splits == 1) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            c1[col + v] = s1[v];
+            c2[col + v] = s2[v];
+        }
+    } else {
+        double *p1 = part + (size_t)blockIdx.y * 2 * cols;
+        double *p2 = p1 + cols;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            p1[col + v] = s1[v];
+            p2[col + v] = s2[v];
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void encode_combine(const double *__restrict__ part,
+                                                           long long cols, int splits,
+                                                           double *__restrict__ c1,
+                                                           double *__restrict__ c2) {
+    const long long col = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (col >= cols) return;
+    double s1 = 0.0, s2 = 0.0;
+    for (int s = 0; s < splits; ++s) {
+        s1 += part[(size_t)s * 2 * cols + col];
+        s2 += part[(size_t)s * 2 * cols + cols + col];
+    }
+    c1[col] = s1;
+    c2[col] = s2;
+}
+
+template <typename T, int VEC>
+hipError_t run(const T *X, long long rows, long long cols, int splits, int wbase, double *c1,
+               double *c2, double *part, hipStream_t st) {
+    const long long threads = (cols + VEC - 1) / VEC;
+    dim3 grid((unsigned)((threads + kThreads - 1) / kThreads), (unsigned)splits);
+    encode_partial<T, VEC><<<grid, kThreads, 0, st>>>(X, rows, cols, wbase, c1, c2, part);
+    if (splits > 1)
+        encode_combine<<<(unsigned)((cols + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+            part, cols, splits, c1, c2);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, double *c2,
+                         void *ws, hipStream_t st) {
+    const Geom &g = pl.g;
+    const long long rows = which == 0 ? g.N : g.M;
+    const long long cols = which == 0 ? g.CHW : (long long)g.K;
+    const int splits = which == 0 ? pl.enc_splits_d : pl.enc_splits_w;
+    double *part = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_enc);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(X);
+    if (g.dtype == FTCNN_F32) {
+        const float *x = static_cast<const float *>(X);
+        if (cols % 4 == 0 && a % 16 == 0) return run<float, 4>(x, rows, cols, splits, g.wbase, c1, c2, part, st);
+        return run<float, 1>(x, rows, cols, splits, g.wbase, c1, c2, part, st);
+    }
+    const uint16_t *x = static_cast<const uint16_t *>(X);
+    if (cols % 8 == 0 && a % 16 == 0) return run<uint16_t, 8>(x, rows, cols, splits, g.wbase, c1, c2, part, st);
+    return run<uint16_t, 1>(x, rows, cols, splits, g.wbase, c1, c2, part, st);
+}
+
+}  // namespace ftcnn

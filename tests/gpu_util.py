@@ -1,0 +1,64 @@
+"""Helpers shared by the GPU tests: device copies, the oracle side of a comparison."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import paper_2003_12203_amd as ft
+import workloads as wl
+from oracle import workflow as wf
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def dev(x: np.ndarray, dtype: str) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    if dtype == "bf16":
+        t = t.to(torch.bfloat16)  # values are already bf16-representable: exact
+    return t.cuda()
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def layer_for(spec: wl.LayerSpec, wbase: int = 0, **policy) -> ft.Layer:
+    pol = ft.make_policy(**policy)
+    return ft.Layer(spec.n, spec.ch, spec.h, spec.w, spec.m, spec.r, spec.s, spec.stride, spec.pad,
+                    spec.dtype, wbase, policy=pol)
+
+
+def assert_close_scaled(got: np.ndarray, ref: np.ndarray, rtol: float, what: str) -> None:
+    """|g - o| <= rtol * (|o| + rms(o)) element by element."""
+    rms = float(np.sqrt(np.mean(ref.astype(np.float64) ** 2))) if ref.size else 0.0
+    err = np.abs(got - ref)
+    lim = rtol * (np.abs(ref) + rms)
+    bad = err > lim
+    if bad.any():
+        idx = np.argwhere(bad)[:5]
+        raise AssertionError(f"{what}: {int(bad.sum())} of {ref.size} elements beyond rtol {rtol}; "
+                             f"first {idx.tolist()} got {got[tuple(idx[0])]} ref {ref[tuple(idx[0])]}")
+
+
+def gpu_flags(layer: ft.Layer) -> np.ndarray:
+    EF = layer.E * layer.F
+    torch.cuda.synchronize()
+    return layer.workspace[:4 * EF].view(torch.int32).cpu().numpy().copy()
+
+
+def to_ft_faults(faults) -> list:
+    out = []
+    for f in faults:
+        d = {"n": f.n, "m": f.m, "x": f.x, "y": f.y, "kind": f.kind}
+        if f.kind == "flip":
+            d["bit"] = f.bit
+        else:
+            d["value"] = f.value
+        out.append(d)
+    return out
+
+
+def oracle_policy_from(pol: ft._lib.Policy, wbase: int = 0) -> wf.Policy:
+    return wf.Policy(rc_on=bool(pol.rc_on), clc_on=bool(pol.clc_on),
+                     repair="recompute" if pol.repair == ft.REPAIR_RECOMPUTE else "checksum",
+                     kappa=pol.kappa, eta=pol.eta, wbase=wbase)

@@ -1,0 +1,93 @@
+"""The C ABI on the host: the library loads, exports every declared entry point, and rejects bad
+arguments before touching a device (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_2003_12203_amd as ft
+from paper_2003_12203_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ftcnn.h")
+
+
+def declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char \*)\s*(ftcnn_\w+)\s*\(", txt, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.load()
+    names = declared()
+    assert len(names) >= 11, names
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(_lib.EXPORTS) == names
+
+
+def test_struct_sizes_match_header_layout():
+    assert C.sizeof(_lib.ConvDesc) == 12 * 4
+    assert C.sizeof(_lib.Checksums) == 15 * 8
+    assert C.sizeof(_lib.ReportHeader) == 14 * 4
+    assert C.sizeof(_lib.Fix) == 5 * 4
+    assert C.sizeof(_lib.Policy) == 4 * 4 + 2 * 8
+    assert C.sizeof(_lib.Fault) == 6 * 4 + 8
+    assert ft.report_bytes(0) == C.sizeof(_lib.ReportHeader)
+    assert ft.report_bytes(7) == C.sizeof(_lib.ReportHeader) + 7 * C.sizeof(_lib.Fix)
+
+
+@pytest.mark.parametrize("h,r,u,p,e", [(227, 11, 4, 0, 55), (224, 7, 2, 3, 112), (56, 1, 2, 0, 28),
+                                       (13, 3, 1, 1, 13), (416, 3, 1, 1, 416), (3, 3, 1, 0, 1)])
+def test_out_shape(h, r, u, p, e):
+    d = ft.make_desc(2, 3, h, h, 4, r, r, u, p)
+    assert ft.out_shape(d) == (e, e)
+    assert ft.workspace_bytes(d) > 0
+    assert ft.workspace_bytes(d) % 256 == 0
+
+
+def test_non_square():
+    d = ft.make_desc(1, 2, 13, 11, 3, 3, 5, 1, 2)
+    assert ft.out_shape(d) == (15, 11)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), -2), (dict(stride=0), -2), (dict(pad=-1), -2), (dict(r=20), -2),
+    (dict(groups=2), -6), (dict(dtype_raw=7), -3), (dict(wbase=2), -1),
+])
+def test_bad_descriptor(kw, code):
+    args = dict(n=2, ch=3, h=8, w=8, m=4, r=3, s=3, stride=1, pad=0, groups=1, dtype=ft.F32, wbase=0)
+    if "dtype_raw" in kw:
+        args["dtype"] = kw.pop("dtype_raw")
+    args.update(kw)
+    d = _lib.ConvDesc(args["n"], args["ch"], args["h"], args["w"], args["m"], args["r"], args["s"],
+                      args["stride"], args["pad"], args["groups"], args["dtype"], args["wbase"])
+    E, F = C.c_int32(), C.c_int32()
+    assert _lib.load().ftcnn_out_shape(C.byref(d), C.byref(E), C.byref(F)) == code
+    assert ft.workspace_bytes(d) == 0
+    assert ft.last_error()
+
+
+def test_null_pointers_rejected_without_launch():
+    L = _lib.load()
+    d = ft.make_desc(2, 3, 8, 8, 4, 3, 3)
+    assert L.ftcnn_conv_fwd(C.byref(d), None, None, None, None) == -1
+    assert L.ftcnn_encode(C.byref(d), 0, None, None, None, None, None) == -1
+    assert L.ftcnn_encode(C.byref(d), 5, C.c_void_p(16), C.c_void_p(16), C.c_void_p(16), None, None) == -1
+    ck = _lib.Checksums()
+    pol = ft.make_policy()
+    assert L.ftcnn_verify(C.byref(d), C.c_void_p(256), C.byref(ck), C.byref(pol), C.c_void_p(256), 4,
+                          C.c_void_p(256), None) == -1
+    bad = ft.make_policy(kappa=-1.0)
+    assert L.ftcnn_verify(C.byref(d), C.c_void_p(256), C.byref(ck), C.byref(bad), C.c_void_p(256), 4,
+                          C.c_void_p(256), None) == -1
+    assert L.ftcnn_checksum_conv(C.byref(d), 1 << 9, None, None, C.byref(ck), None) == -1
+    f = (_lib.Fault * 1)(_lib.Fault(5, 0, 0, 0, 0, 3, 0.0))
+    assert L.ftcnn_inject(C.byref(d), C.c_void_p(256), f, 1, None) == -1   # n out of range
+    f = (_lib.Fault * 1)(_lib.Fault(0, 0, 0, 0, 0, 40, 0.0))
+    assert L.ftcnn_inject(C.byref(d), C.c_void_p(256), f, 1, None) == -1   # bit out of range
+    assert L.ftcnn_inject(C.byref(d), C.c_void_p(256), f, 65, None) == -1
+    ws_mis = C.c_void_p(256 + 8)
+    assert L.ftcnn_verify(C.byref(d), C.c_void_p(256), C.byref(ck), C.byref(pol), C.c_void_p(256), 4,
+                          ws_mis, None) == -1  # ck arrays missing are reported first

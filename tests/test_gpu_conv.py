@@ -1,0 +1,88 @@
+"""GPU parity of the main convolution (eq. 1) against the oracle, every layer shape of the workloads."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from gpu_util import TOL, assert_close_scaled, dev, host, layer_for
+from oracle import core
+from oracle import workflow as wf
+
+pytestmark = pytest.mark.gpu
+
+
+def _shapes():
+    """Distinct layer shapes of all workloads, shrunk (batch, then spatial crop) to about a GFLOP."""
+    seen, out = set(), []
+    cfgs = wl.configs() + [wl.vgg19_bf16()]
+    for cfg in cfgs:
+        for li, L in enumerate(cfg.layers):
+            key = (L.ch, L.h, L.m, L.r, L.stride, L.pad, L.dtype)
+            if key in seen:
+                continue
+            seen.add(key)
+            spec = L
+            for n in (3, 2, 1):
+                spec = spec.with_(n=min(n, L.n))
+                E = core.out_extent(spec.h, spec.r, spec.stride, spec.pad)
+                if 2 * spec.n * spec.m * E * E * spec.ch * spec.r * spec.s <= 1.5e9:
+                    break
+            h = spec.h
+            while True:
+                E = core.out_extent(h, spec.r, spec.stride, spec.pad)
+                if 2 * spec.n * spec.m * E * E * spec.ch * spec.r * spec.s <= 1.5e9 or h <= 2 * spec.r:
+                    break
+                h = int(h * 0.8)
+            spec = spec.with_(h=h, w=h)
+            out.append(pytest.param(cfg, li, spec, id=f"{cfg.name}-{L.name}-n{spec.n}-h{spec.h}"))
+    return out
+
+
+@pytest.mark.parametrize("cfg,li,spec", _shapes())
+def test_conv_matches_oracle(cfg, li, spec):
+    D = wl.gen_d(cfg, li, spec)
+    W = wl.gen_w(cfg, li, spec)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
+    O = lay.empty_output()
+    lay.conv(Dd, Wd, O)
+    torch.cuda.synchronize()
+    ref = wf.store(core.conv(D, W, spec.stride, spec.pad), spec.dtype)
+    assert_close_scaled(host(O), ref, TOL[spec.dtype], f"O {spec}")
+
+
+@pytest.mark.parametrize("shape", [
+    # n, ch, h, m, r, stride, pad: ragged pixel tails, partial M tiles, K tails, 1x1 outputs
+    (3, 16, 10, 5, 3, 1, 1),
+    (1, 3, 11, 96, 11, 4, 0),
+    (2, 7, 9, 33, 3, 2, 1),
+    (2, 5, 3, 7, 3, 1, 0),       # E = 1
+    (1, 1, 1, 1, 1, 1, 0),       # a single multiply
+    (4, 64, 7, 130, 1, 1, 0),    # M just past a 128 tile
+    (2, 8, 13, 64, 5, 3, 2),
+])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv_integer_inputs_bitwise(shape, dtype):
+    """Integer inputs keep every partial sum exact, so the GPU result must equal the oracle bit for bit."""
+    n, ch, h, m, r, u, p = shape
+    spec = wl.LayerSpec("int", n, ch, h, h, m, r, r, u, p, dtype)
+    D = wl.gen_int_d(spec, seed=sum(shape))
+    W = wl.gen_int_w(spec, seed=sum(shape))
+    lay = layer_for(spec)
+    O = lay.empty_output()
+    lay.conv(dev(D, dtype), dev(W, dtype), O)
+    torch.cuda.synchronize()
+    ref = wf.store(core.conv(D, W, u, p), dtype)  # exact sums, one rounding to the dtype on both sides
+    np.testing.assert_array_equal(host(O), ref)
+
+
+def test_conv_deterministic():
+    cfg = wl.config(1)
+    spec = cfg.layers[2].with_(n=4)
+    lay = layer_for(spec)
+    D, W = dev(wl.gen_d(cfg, 2, spec), "f32"), dev(wl.gen_w(cfg, 2, spec), "f32")
+    O1, O2 = lay.empty_output(), lay.empty_output()
+    lay.conv(D, W, O1)
+    lay.conv(D, W, O2)
+    torch.cuda.synchronize()
+    assert torch.equal(O1, O2)
