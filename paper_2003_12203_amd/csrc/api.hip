@@ -55,7 +55,9 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     const long long K = (long long)d->ch * d->r * d->s;
     const long long EF = (long long)g.E * g.F;
     const long long CHW = (long long)d->ch * d->h * d->w;
-    if (K > (1LL << 30) || EF > (1LL << 30) || CHW > (1LL << 30) || d->m > (1 << 20) || d->n > (1 << 20))
+    if (K > (1LL << 30) || EF > (1LL << 30) || CHW > (1LL << 30) || d->m > (1 << 20) || d->n > (1 << 20) ||
+        (long long)d->n * d->m > (1LL << 30) || (long long)d->n * CHW >= (1LL << 31) ||
+        (long long)d->m * K >= (1LL << 31))
         return fail(FTCNN_E_SHAPE, "dimension beyond the supported range");
     g.K = (int)K;
     g.EF = (int)EF;
@@ -66,13 +68,19 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
 
     const int vec = g.dtype == FTCNN_F32 ? 4 : 8;
     // input checksums
-    pl->enc_splits_d = row_splits(g.N, ceil_div(ceil_div(CHW, vec), kThreads), 1024, 4);
-    pl->enc_splits_w = row_splits(g.M, ceil_div(ceil_div(K, vec), kThreads), 1024, 4);
+    pl->enc_splits_d = row_splits(g.N, ceil_div(ceil_div(CHW, vec), kThreads), 512, 8);
+    pl->enc_splits_w = row_splits(g.M, ceil_div(ceil_div(K, vec), kThreads), 512, 8);
     // verification
     const long long cols_v = ceil_div(EF, EF % vec == 0 ? vec : 1);
     const long long ctt = cols_v < kThreads ? cols_v : kThreads;
     pl->ver_cols_per_block = (int)ctt;
-    pl->ver_splits = row_splits((long long)g.N * g.M, ceil_div(cols_v, ctt), 768, 128);
+    // enough blocks to fill the chip, while the float64 split partials stay a few percent of O
+    const long long rows_o = (long long)g.N * g.M;
+    const long long o_bytes = rows_o * EF * (g.dtype == FTCNN_F32 ? 4 : 2);
+    const long long part_budget = o_bytes / 20 > (4LL << 20) ? o_bytes / 20 : (4LL << 20);
+    const long long part_cap = part_budget / (32 * EF);
+    pl->ver_splits = row_splits(rows_o, ceil_div(cols_v, ctt), 1024, 32);
+    if (pl->ver_splits > part_cap) pl->ver_splits = part_cap > 1 ? (int)part_cap : 1;
     // correction
     pl->corr_blocks = 256;
     const long long L = g.M > g.N ? g.M : g.N;

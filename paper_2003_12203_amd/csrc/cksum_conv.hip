@@ -48,26 +48,53 @@ __device__ inline void window3(const Geom &g, const TA *a1, const TA *a2, const 
     }
 }
 
-// Co5, Co6, Co7 at every position; `wave` selects one wave per position.
-template <bool WAVE>
+// Co5, Co6, Co7 at every position.  TPP threads share one position and stride
+// over the flat k = (c, r, s) index; their partial sums meet in a fixed
+// butterfly (and, for TPP = 256, in wave order through LDS).
+template <int TPP>
 __global__ __launch_bounds__(kThreads) void coc_kernel(Geom g, const double *__restrict__ cd1,
                                                        const double *__restrict__ cd2,
                                                        const double *__restrict__ cw1,
                                                        const double *__restrict__ cw2, double *co5,
                                                        double *co6, double *co7) {
-    const int per_block = WAVE ? kThreads / 64 : kThreads;
-    const int p = blockIdx.x * per_block + (WAVE ? threadIdx.x / 64 : threadIdx.x);
-    if (p >= g.EF) return;
-    const int lane = WAVE ? (threadIdx.x & 63) : 0;
-    const int x = p / g.F, y = p - (p / g.F) * g.F;
+    constexpr int G = TPP < 64 ? TPP : 64;  // lanes combined by shuffles
+    const int lane = threadIdx.x % TPP;
+    const int p = blockIdx.x * (kThreads / TPP) + threadIdx.x / TPP;
     double s11 = 0.0, s12 = 0.0, s21 = 0.0;
-    window3<double, double>(g, cd1, cd2, cw1, cw2, x, y, lane, WAVE ? 64 : 1, s11, s12, s21);
-    if (WAVE) {
-        s11 = wave_sum(s11);
-        s12 = wave_sum(s12);
-        s21 = wave_sum(s21);
+    if (p < g.EF) {
+        const int x = p / g.F, y = p - (p / g.F) * g.F;
+        const int RS = g.R * g.S;
+        for (int k = lane; k < g.K; k += TPP) {
+            const int c = k / RS, rem = k - c * RS, r = rem / g.S, s = rem - r * g.S;
+            const int ih = g.U * x + r - g.P, iw = g.U * y + s - g.P;
+            if (ih < 0 || ih >= g.H || iw < 0 || iw >= g.W) continue;
+            const long long ia = ((long long)c * g.H + ih) * g.W + iw;
+            const double x1 = cd1[ia], w1 = cw1[k];
+            s11 = fma(x1, w1, s11);
+            if (cw2) s12 = fma(x1, cw2[k], s12);
+            if (cd2) s21 = fma(cd2[ia], w1, s21);
+        }
     }
-    if (lane == 0) {
+#pragma unroll
+    for (int o = G / 2; o > 0; o >>= 1) {
+        s11 += __shfl_xor(s11, o, 64);
+        s12 += __shfl_xor(s12, o, 64);
+        s21 += __shfl_xor(s21, o, 64);
+    }
+    if constexpr (TPP == kThreads) {
+        __shared__ double red[3][kThreads / 64];
+        const int w = threadIdx.x / 64;
+        if ((threadIdx.x & 63) == 0) {
+            red[0][w] = s11;
+            red[1][w] = s12;
+            red[2][w] = s21;
+        }
+        __syncthreads();
+        s11 = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+        s12 = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+        s21 = ((red[2][0] + red[2][1]) + red[2][2]) + red[2][3];
+    }
+    if (p < g.EF && lane == 0) {
         if (co5) co5[p] = s11;
         if (co6) co6[p] = s12;
         if (co7) co7[p] = s21;
@@ -169,10 +196,13 @@ hipError_t launch_checksum_conv(const Plan &pl, uint32_t which, const void *D, c
         double *o7 = (which & FTCNN_CO7) ? ck.co7 : nullptr;
         const double *cw2 = o6 ? ck.cw2 : nullptr;
         const double *cd2 = o7 ? ck.cd2 : nullptr;
-        if (wave)
-            coc_kernel<true><<<blocks_for(g.EF, true), kThreads, 0, st>>>(g, ck.cd1, cd2, ck.cw1, cw2, o5, o6, o7);
-        else
-            coc_kernel<false><<<blocks_for(g.EF, false), kThreads, 0, st>>>(g, ck.cd1, cd2, ck.cw1, cw2, o5, o6, o7);
+#define COC(TPP)                                                                                    \
+    coc_kernel<TPP><<<(unsigned)((g.EF + kThreads / TPP - 1) / (kThreads / TPP)), kThreads, 0, st>>>( \
+        g, ck.cd1, cd2, ck.cw1, cw2, o5, o6, o7)
+        if (g.K <= 64) COC(16);
+        else if (g.EF <= 4096) COC(256);
+        else COC(64);
+#undef COC
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

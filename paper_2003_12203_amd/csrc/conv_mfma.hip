@@ -32,23 +32,25 @@ __device__ inline int xcd_tile(int bid, int total) {
 }
 
 // Element-type traits: fp32 uses v_mfma_f32_32x32x2_f32 (2 k per instruction),
-// bf16 uses v_mfma_f32_32x32x16_bf16 (16 k per instruction).
-struct F32T {
+// bf16 uses v_mfma_f32_32x32x16_bf16 (16 k per instruction).  TK_ is the k
+// extent of one LDS chunk; rows are padded by 16 bytes against bank conflicts.
+template <int TK_> struct F32T {
     using T = float;
-    static constexpr int TK = 16;      // k per chunk
-    static constexpr int LDK = 20;     // LDS row stride in elements (16 + 4 pad)
-    static constexpr int VEC = 4;      // elements per 16-byte A load
+    static constexpr int TK = TK_;
+    static constexpr int LDK = TK_ + 4;
+    static constexpr int VEC = 4;      // elements per 16-byte load
 };
-struct BF16T {
+template <int TK_> struct BF16T {
     using T = uint16_t;
-    static constexpr int TK = 32;
-    static constexpr int LDK = 40;     // 32 + 8 pad (80-byte rows)
+    static constexpr int TK = TK_;
+    static constexpr int LDK = TK_ + 8;
     static constexpr int VEC = 8;
 };
 
-template <typename Tr, int WM, int WP, int FM, int FP>
+template <typename Tr, int WM, int WP, int FM, int FP, bool KVEC_ = true>
 struct Cfg {
     using T = typename Tr::T;
+    static constexpr bool KVEC = KVEC_;   // W rows 16-byte aligned: whole-slot weight loads
     static constexpr int NT = 64 * WM * WP;
     static constexpr int TM = WM * FM * 32;
     static constexpr int TP = WP * FP * 32;
@@ -60,8 +62,9 @@ struct Cfg {
     static constexpr int KG = NT / TP;                               // threads per pixel along k
     static constexpr int KR = TK / KG;                               // k per thread in the gather
     static_assert(NT % TP == 0 && TK % KG == 0 && KR % VEC == 0, "tile shape");
+    static_assert(KR <= 32 && A_PER * VEC <= 32, "gather masks are 32-bit");
     static constexpr size_t LDS_BYTES = 2ull * (TM + TP) * LDK * sizeof(T);
-    static_assert(LDS_BYTES <= 65536, "tile exceeds the default LDS allocation");
+    static_assert(LDS_BYTES <= 160 * 1024, "tile exceeds the LDS of a CU");
 };
 
 // 16 bytes of elements, moved between global memory, registers and LDS as one unit.
@@ -70,67 +73,117 @@ template <typename T, int VEC> union Pack {
     T e[VEC];
 };
 
+// Per-lane constants of the A (weights) gather: which 16-byte slots of the
+// TM x TK tile this lane moves, and where each slot's row starts in W.
+template <typename C> struct ASlots {
+    int base[C::A_PER];   // element offset of the slot's first k in W, -1 if the row is past M
+    int kq[C::A_PER];     // k offset of the slot inside the chunk
+};
+
 template <typename C>
-__device__ inline void load_a(const typename C::T *__restrict__ Wt, const Geom &g, int m0, int kbase,
-                              int tid, bool kvec, Pack<typename C::T, C::VEC> (&ra)[C::A_PER]) {
-    using T = typename C::T;
+__device__ inline void a_slots(const Geom &g, int m0, int tid, ASlots<C> &as) {
 #pragma unroll
     for (int i = 0; i < C::A_PER; ++i) {
         const int slot = tid + i * C::NT;
         const int row = slot / (C::TK / C::VEC);
-        const int kq = slot % (C::TK / C::VEC);
         const int m = m0 + row;
-        const int k = kbase + kq * C::VEC;
-        if (slot < C::A_SLOTS && m < g.M && k < g.K) {
-            const T *src = Wt + (long long)m * g.K + k;
-            if (kvec && k + C::VEC <= g.K) {
-                ra[i].q = *reinterpret_cast<const uint4 *>(src);
-            } else {
-#pragma unroll
-                for (int v = 0; v < C::VEC; ++v) ra[i].e[v] = (k + v < g.K) ? src[v] : T(0);
-            }
-        } else {
-            ra[i].q = make_uint4(0u, 0u, 0u, 0u);
-        }
+        as.kq[i] = (slot % (C::TK / C::VEC)) * C::VEC;
+        as.base[i] = (slot < C::A_SLOTS && m < g.M) ? m * g.K + as.kq[i] : -1;
     }
 }
 
+// Loads are unconditional (a masked lane reads element 0 and discards it), so
+// the whole gather is straight-line code the scheduler can interleave with MFMAs.
+// The masks are applied only when the registers go to LDS (after the MFMAs of
+// the current chunk), so no wait for these loads sits in front of the MFMAs.
 template <typename C>
-__device__ inline void load_b(const typename C::T *__restrict__ Dt, const Geom &g, int kstart,
-                              bool pvalid, long long dbase, int ih0, int iw0,
-                              Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+__device__ inline uint32_t load_a(const typename C::T *__restrict__ Wt, const Geom &g, int kbase, bool,
+                                  const ASlots<C> &as, Pack<typename C::T, C::VEC> (&ra)[C::A_PER]) {
+    uint32_t mask = 0;
+#pragma unroll
+    for (int i = 0; i < C::A_PER; ++i) {
+        const int k = kbase + as.kq[i];
+        if constexpr (C::KVEC) {
+            // W rows start on 16-byte boundaries (K % VEC == 0, aligned base): index
+            // through a uint4 pointer so the load is one global_load_dwordx4
+            const bool ok = (as.base[i] >= 0) & (k < g.K);
+            const uint4 *w4 = reinterpret_cast<const uint4 *>(Wt);
+            ra[i].q = w4[ok ? (as.base[i] + kbase) / C::VEC : 0];
+            mask |= (ok ? ((1u << C::VEC) - 1u) : 0u) << (i * C::VEC);
+        } else {
+#pragma unroll
+            for (int v = 0; v < C::VEC; ++v) {
+                const bool ok = (as.base[i] >= 0) & (k + v < g.K);
+                ra[i].e[v] = Wt[ok ? as.base[i] + kbase + v : 0];
+                mask |= (ok ? 1u : 0u) << (i * C::VEC + v);
+            }
+        }
+    }
+    return mask;
+}
+
+// The im2col gather of B: this lane's pixel is fixed (lane_base = n*C*H*W +
+// ih0*W + iw0); the run of KR consecutive k is the same for the whole wave, so
+// (c, r, s) and the k part of the offset live in scalar registers.
+template <typename C>
+__device__ inline uint32_t load_b(const typename C::T *__restrict__ Dt, const Geom &g, int kstart_lane,
+                                  bool pvalid, int lane_base, int ih0, int iw0,
+                                  Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+    uint32_t mask = 0;
     using T = typename C::T;
+    const int kstart = __builtin_amdgcn_readfirstlane(kstart_lane);
     const int RS = g.R * g.S;
     int c = kstart / RS;
-    int rem = kstart - c * RS;
+    const int rem = kstart - c * RS;
     int r = rem / g.S;
     int s = rem - r * g.S;
-    const long long HW = (long long)g.H * g.W;
+    const int HW = g.H * g.W;
+    int koff = c * HW + r * g.W + s;
+    const int wrap_s = g.W - g.S, wrap_r = HW - g.R * g.W;
 #pragma unroll
     for (int j = 0; j < C::KR; ++j) {
         const int ih = ih0 + r, iw = iw0 + s;
-        const bool ok = pvalid && (kstart + j < g.K) && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W;
-        rb[j / C::VEC].e[j % C::VEC] = ok ? Dt[dbase + c * HW + (long long)ih * g.W + iw] : T(0);
-        if (++s == g.S) {
-            s = 0;
-            if (++r == g.R) { r = 0; ++c; }
-        }
+        // bitwise, not short-circuit: no branches in the gather
+        const bool ok = pvalid & (kstart + j < g.K) & ((unsigned)ih < (unsigned)g.H) &
+                        ((unsigned)iw < (unsigned)g.W);
+        rb[j / C::VEC].e[j % C::VEC] = Dt[ok ? lane_base + koff : 0];
+        mask |= (ok ? 1u : 0u) << j;
+        // advance (c, r, s) by one k with selects (scalar registers)
+        ++s;
+        ++koff;
+        const bool ws = s == g.S;
+        s = ws ? 0 : s;
+        koff += ws ? wrap_s : 0;
+        r += ws ? 1 : 0;
+        const bool wr = r == g.R;
+        r = wr ? 0 : r;
+        koff += wr ? wrap_r : 0;
+        c += wr ? 1 : 0;
     }
+    return mask;
 }
 
 template <typename C>
 __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
-                                 const Pack<typename C::T, C::VEC> (&ra)[C::A_PER],
-                                 const Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC], int bp, int bkg) {
+                                 Pack<typename C::T, C::VEC> (&ra)[C::A_PER], uint32_t amask,
+                                 Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC], uint32_t bmask,
+                                 int bp, int bkg) {
+    using T = typename C::T;
 #pragma unroll
     for (int i = 0; i < C::A_PER; ++i) {
         const int slot = tid + i * C::NT;
-        if (slot < C::A_SLOTS) {
+        if (C::A_SLOTS % C::NT == 0 || slot < C::A_SLOTS) {
+#pragma unroll
+            for (int v = 0; v < C::VEC; ++v)
+                ra[i].e[v] = ((amask >> (i * C::VEC + v)) & 1u) ? ra[i].e[v] : T(0);
             const int row = slot / (C::TK / C::VEC);
             const int kq = slot % (C::TK / C::VEC);
             *reinterpret_cast<uint4 *>(&As[row * C::LDK + kq * C::VEC]) = ra[i].q;
         }
     }
+#pragma unroll
+    for (int j = 0; j < C::KR; ++j)
+        rb[j / C::VEC].e[j % C::VEC] = ((bmask >> j) & 1u) ? rb[j / C::VEC].e[j % C::VEC] : T(0);
 #pragma unroll
     for (int j = 0; j < C::KR; j += C::VEC)
         *reinterpret_cast<uint4 *>(&Bs[bp * C::LDK + bkg * C::KR + j]) = rb[j / C::VEC].q;
@@ -139,19 +192,20 @@ __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
 // One chunk of MFMAs from LDS.  Within a chunk, lanes 0-31 take the first half
 // of the k range and lanes 32-63 the second half; A and B use the same
 // assignment, so every k of the chunk is summed exactly once.
-template <int FM, int FP>
+template <int TK, int FM, int FP>
 __device__ inline void mma_f32(const float *As, const float *Bs, int lane, int arow0, int brow0,
                                floatx16 (&acc)[FM][FP]) {
+    constexpr int LDK = F32T<TK>::LDK;
     const int l32 = lane & 31, h = lane >> 5;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < TK / 8; ++q) {
         floatx4 a[FM], b[FP];
 #pragma unroll
         for (int i = 0; i < FM; ++i)
-            a[i] = *reinterpret_cast<const floatx4 *>(&As[(arow0 + i * 32 + l32) * F32T::LDK + h * 8 + q * 4]);
+            a[i] = *reinterpret_cast<const floatx4 *>(&As[(arow0 + i * 32 + l32) * LDK + h * (TK / 2) + q * 4]);
 #pragma unroll
         for (int j = 0; j < FP; ++j)
-            b[j] = *reinterpret_cast<const floatx4 *>(&Bs[(brow0 + j * 32 + l32) * F32T::LDK + h * 8 + q * 4]);
+            b[j] = *reinterpret_cast<const floatx4 *>(&Bs[(brow0 + j * 32 + l32) * LDK + h * (TK / 2) + q * 4]);
 #pragma unroll
         for (int t = 0; t < 4; ++t)
 #pragma unroll
@@ -162,21 +216,22 @@ __device__ inline void mma_f32(const float *As, const float *Bs, int lane, int a
     }
 }
 
-template <int FM, int FP>
+template <int TK, int FM, int FP>
 __device__ inline void mma_bf16(const uint16_t *As, const uint16_t *Bs, int lane, int arow0, int brow0,
                                 floatx16 (&acc)[FM][FP]) {
+    constexpr int LDK = BF16T<TK>::LDK;
     const int l32 = lane & 31, h = lane >> 5;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < TK / 16; ++q) {
         bf16x8 a[FM], b[FP];
 #pragma unroll
         for (int i = 0; i < FM; ++i)
             a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(
-                                                  &As[(arow0 + i * 32 + l32) * BF16T::LDK + h * 16 + q * 8]));
+                                                  &As[(arow0 + i * 32 + l32) * LDK + h * (TK / 2) + q * 8]));
 #pragma unroll
         for (int j = 0; j < FP; ++j)
             b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(
-                                                  &Bs[(brow0 + j * 32 + l32) * BF16T::LDK + h * 16 + q * 8]));
+                                                  &Bs[(brow0 + j * 32 + l32) * LDK + h * (TK / 2) + q * 8]));
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -185,12 +240,126 @@ __device__ inline void mma_bf16(const uint16_t *As, const uint16_t *Bs, int lane
     }
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP>
+// Stateful form of the B gather, so that its elements can be issued one at a
+// time between MFMAs: (c, r, s) and the k offset advance in scalar registers.
+template <typename C> struct BGather {
+    int kstart, c, r, s, koff;
+    uint32_t mask;
+    __device__ inline void begin(const Geom &g, int kstart_lane) {
+        kstart = __builtin_amdgcn_readfirstlane(kstart_lane);
+        const int RS = g.R * g.S;
+        c = kstart / RS;
+        const int rem = kstart - c * RS;
+        r = rem / g.S;
+        s = rem - r * g.S;
+        koff = c * g.H * g.W + r * g.W + s;
+        mask = 0;
+    }
+    __device__ inline void element(const typename C::T *__restrict__ Dt, const Geom &g, int j, bool pvalid,
+                                   int lane_base, int ih0, int iw0, Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+        const int ih = ih0 + r, iw = iw0 + s;
+        const bool ok = pvalid & (kstart + j < g.K) & ((unsigned)ih < (unsigned)g.H) &
+                        ((unsigned)iw < (unsigned)g.W);
+        rb[j / C::VEC].e[j % C::VEC] = Dt[ok ? lane_base + koff : 0];
+        mask |= (ok ? 1u : 0u) << j;
+        ++s;
+        ++koff;
+        const bool ws = s == g.S;
+        s = ws ? 0 : s;
+        koff += ws ? g.W - g.S : 0;
+        r += ws ? 1 : 0;
+        const bool wr = r == g.R;
+        r = wr ? 0 : r;
+        koff += wr ? g.H * g.W - g.R * g.W : 0;
+        c += wr ? 1 : 0;
+    }
+};
+
+// One fp32 chunk with the next chunk's gather woven in: after every k-step
+// (FM x FP MFMAs) the wave issues its share of the gather, so the vector ALU
+// and the load pipeline run while the matrix core works.  sched_barrier(0)
+// keeps the compiler from regrouping the two streams.
+template <typename C, int FM, int FP, bool NEXT>
+__device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int arow0, int brow0,
+                                 floatx16 (&acc)[FM][FP], const typename C::T *__restrict__ Dt,
+                                 const typename C::T *__restrict__ Wt, const Geom &g, int kb_next, bool kvec,
+                                 const ASlots<C> &as, Pack<typename C::T, C::VEC> (&ra)[C::A_PER], uint32_t &amask,
+                                 BGather<C> &bg, int bkg, bool pvalid, int lane_base, int ih0, int iw0,
+                                 Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+    constexpr int TK = C::TK, LDK = C::LDK, STEPS = TK / 2;
+    const int l32 = lane & 31, h = lane >> 5;
+    floatx4 a[TK / 8][FM], b[TK / 8][FP];
+#pragma unroll
+    for (int q = 0; q < TK / 8; ++q) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+            a[q][i] = *reinterpret_cast<const floatx4 *>(&As[(arow0 + i * 32 + l32) * LDK + h * (TK / 2) + q * 4]);
+#pragma unroll
+        for (int j = 0; j < FP; ++j)
+            b[q][j] = *reinterpret_cast<const floatx4 *>(&Bs[(brow0 + j * 32 + l32) * LDK + h * (TK / 2) + q * 4]);
+    }
+    if constexpr (NEXT) {
+        amask = load_a<C>(Wt, g, kb_next, kvec, as, ra);
+        bg.begin(g, kb_next + bkg * C::KR);
+    }
+#pragma unroll
+    for (int t = 0; t < STEPS; ++t) {
+        const int q = t / 4, tt = t % 4;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FP; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][i][tt], b[q][j][tt], acc[i][j], 0, 0, 0);
+        if constexpr (NEXT) {
+            __builtin_amdgcn_sched_barrier(0);
+            const int E0 = t * C::KR / STEPS, E1 = (t + 1) * C::KR / STEPS;  // folded by unrolling
+#pragma unroll
+            for (int e = E0; e < E1; ++e) bg.element(Dt, g, e, pvalid, lane_base, ih0, iw0, rb);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// Instruction interleave for one K chunk: the next chunk's gather (VALU, SALU
+// and VMEM) is spread between this chunk's MFMAs, so the vector ALU and the
+// memory pipeline work while the matrix core is busy.
+template <int SCHED, int NMFMA, int NVMEM>
+__device__ inline void interleave() {
+    if constexpr (SCHED == 1) {
+#pragma unroll
+        for (int i = 0; i < NMFMA; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
+            if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);      // VALU
+            __builtin_amdgcn_sched_group_barrier(0x004, 2, 0);      // SALU
+        }
+    } else if constexpr (SCHED == 2) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);          // first LDS operand reads
+#pragma unroll
+        for (int i = 0; i < NMFMA; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < 4) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+            __builtin_amdgcn_sched_group_barrier(0x004, 3, 0);
+        }
+    } else if constexpr (SCHED == 3) {
+#pragma unroll
+        for (int i = 0; i < NMFMA; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i % 2 == 0 && i / 2 < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x004, 1, 0);
+        }
+    }
+}
+
+template <typename Tr, int WM, int WP, int FM, int FP, int SCHED = 0, bool KVEC = true>
 __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T *__restrict__ D,
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
-                                                            int tiles_m, int tiles_total, int kvec) {
-    using C = Cfg<Tr, WM, WP, FM, FP>;
+                                                            int tiles_m, int tiles_total, int m_major) {
+    using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
     using T = typename C::T;
     extern __shared__ __align__(16) unsigned char smem[];
     T *As0 = reinterpret_cast<T *>(smem);
@@ -199,24 +368,31 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wp = wave / WM;
+    // logical tile order: pixel-major keeps the M tiles of one pixel tile on one
+    // XCD (its L2 serves the repeated D reads); M-major keeps one slab of W
+    // resident per XCD instead (preferred when W is larger than an XCD's L2)
     const int tile = xcd_tile(blockIdx.x, tiles_total);
-    const int m0 = (tile % tiles_m) * C::TM;
-    const long long p0 = (long long)(tile / tiles_m) * C::TP;
+    const int tiles_p = tiles_total / tiles_m;
+    const int mt = m_major ? tile / tiles_p : tile % tiles_m;
+    const int pt = m_major ? tile % tiles_p : tile / tiles_m;
+    const int m0 = mt * C::TM;
+    const long long p0 = (long long)pt * C::TP;
 
     // this thread's im2col pixel (fixed over the K loop)
     const int bp = tid % C::TP, bkg = tid / C::TP;
     const long long pg = p0 + bp;
     const bool pvalid = pg < g.P_total;
-    long long dbase = 0;
-    int ih0 = 0, iw0 = 0;
+    int lane_base = 0, ih0 = 0, iw0 = 0;
     if (pvalid) {
-        const long long n = pg / g.EF;
-        const int pix = (int)(pg - n * g.EF);
+        const int n = (int)(pg / g.EF);
+        const int pix = (int)(pg - (long long)n * g.EF);
         const int x = pix / g.F, y = pix - (pix / g.F) * g.F;
-        dbase = n * g.CHW;
         ih0 = g.U * x - g.P;
         iw0 = g.U * y - g.P;
+        lane_base = n * (int)g.CHW + ih0 * g.W + iw0;
     }
+    ASlots<C> as;
+    a_slots<C>(g, m0, tid, as);
 
     floatx16 acc[FM][FP];
 #pragma unroll
@@ -229,31 +405,89 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     Pack<T, C::VEC> ra[C::A_PER];
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
-    load_a<C>(Wt, g, m0, 0, tid, kvec != 0, ra);
-    load_b<C>(D, g, bkg * C::KR, pvalid, dbase, ih0, iw0, rb);
-    store_lds<C>(As0, Bs0, tid, ra, rb, bp, bkg);
+    uint32_t amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
+    uint32_t bmask = load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+    store_lds<C>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
     __syncthreads();
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    for (int kc = 0; kc < nchunks; ++kc) {
-        const int buf = kc & 1;
-        const bool more = kc + 1 < nchunks;
-        if (more) {
-            const int kb = (kc + 1) * C::TK;
-            load_a<C>(Wt, g, m0, kb, tid, kvec != 0, ra);
-            load_b<C>(D, g, kb + bkg * C::KR, pvalid, dbase, ih0, iw0, rb);
-        }
+    auto mma = [&](int buf) {
         const T *As = As0 + buf * C::TM * C::LDK;
         const T *Bs = Bs0 + buf * C::TP * C::LDK;
         if constexpr (sizeof(T) == 4)
-            mma_f32<FM, FP>(reinterpret_cast<const float *>(As), reinterpret_cast<const float *>(Bs),
-                            lane, arow0, brow0, acc);
+            mma_f32<C::TK, FM, FP>(reinterpret_cast<const float *>(As), reinterpret_cast<const float *>(Bs),
+                                   lane, arow0, brow0, acc);
         else
-            mma_bf16<FM, FP>(reinterpret_cast<const uint16_t *>(As), reinterpret_cast<const uint16_t *>(Bs),
-                             lane, arow0, brow0, acc);
-        if (more) store_lds<C>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra,
-                               rb, bp, bkg);
-        __syncthreads();
+            mma_bf16<C::TK, FM, FP>(reinterpret_cast<const uint16_t *>(As),
+                                    reinterpret_cast<const uint16_t *>(Bs), lane, arow0, brow0, acc);
+    };
+    constexpr int kMfmaPerChunk = FM * FP * (sizeof(T) == 4 ? C::TK / 2 : C::TK / 16);
+    constexpr int kVmemPerChunk = C::A_PER * (sizeof(T) == 4 ? 1 : 1) + C::KR;
+    // every chunk but the last: fetch the next one while the MFMAs consume this one
+    if constexpr (SCHED == 4 && sizeof(T) == 4) {
+        BGather<C> bg;
+        for (int kc = 0; kc + 1 < nchunks; ++kc) {
+            const int buf = kc & 1;
+            chunk_f32<C, FM, FP, true>(reinterpret_cast<const float *>(As0 + buf * C::TM * C::LDK),
+                                       reinterpret_cast<const float *>(Bs0 + buf * C::TP * C::LDK), lane, arow0,
+                                       brow0, acc, D, Wt, g, (kc + 1) * C::TK, KVEC, as, ra, amask, bg, bkg,
+                                       pvalid, lane_base, ih0, iw0, rb);
+            store_lds<C>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
+                         bg.mask, bp, bkg);
+            __syncthreads();
+        }
+        chunk_f32<C, FM, FP, false>(reinterpret_cast<const float *>(As0 + ((nchunks - 1) & 1) * C::TM * C::LDK),
+                                    reinterpret_cast<const float *>(Bs0 + ((nchunks - 1) & 1) * C::TP * C::LDK),
+                                    lane, arow0, brow0, acc, D, Wt, g, 0, KVEC, as, ra, amask, bg, bkg, pvalid,
+                                    lane_base, ih0, iw0, rb);
+    } else if constexpr (SCHED == 5) {
+        // two chunks in flight: registers hold chunks kc+1 and kc+2 while chunk kc is consumed
+        Pack<T, C::VEC> ra2[C::A_PER];
+        Pack<T, C::VEC> rb2[C::KR / C::VEC];
+        uint32_t amask2 = 0, bmask2 = 0;
+        if (nchunks > 1) {
+            amask2 = load_a<C>(Wt, g, C::TK, KVEC, as, ra2);
+            bmask2 = load_b<C>(D, g, C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
+        }
+        int kc = 0;
+        for (; kc + 2 < nchunks; kc += 2) {
+            // even step: regs2 hold kc+1; fetch kc+2 into regs
+            amask = load_a<C>(Wt, g, (kc + 2) * C::TK, KVEC, as, ra);
+            bmask = load_b<C>(D, g, (kc + 2) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+            mma(0);
+            store_lds<C>(As0 + C::TM * C::LDK, Bs0 + C::TP * C::LDK, tid, ra2, amask2, rb2, bmask2, bp, bkg);
+            __syncthreads();
+            // odd step: regs hold kc+2; fetch kc+3 into regs2
+            if (kc + 3 < nchunks) {
+                amask2 = load_a<C>(Wt, g, (kc + 3) * C::TK, KVEC, as, ra2);
+                bmask2 = load_b<C>(D, g, (kc + 3) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
+            }
+            mma(1);
+            store_lds<C>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
+            __syncthreads();
+        }
+        // kc is even; chunks kc (in LDS 0) and possibly kc+1 (in regs2) remain
+        if (kc + 1 < nchunks) {
+            mma(0);
+            store_lds<C>(As0 + C::TM * C::LDK, Bs0 + C::TP * C::LDK, tid, ra2, amask2, rb2, bmask2, bp, bkg);
+            __syncthreads();
+            mma(1);
+        } else {
+            mma(0);
+        }
+    } else {
+        for (int kc = 0; kc + 1 < nchunks; ++kc) {
+            const int buf = kc & 1;
+            const int kb = (kc + 1) * C::TK;
+            amask = load_a<C>(Wt, g, kb, KVEC, as, ra);
+            bmask = load_b<C>(D, g, kb + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+            mma(buf);
+            store_lds<C>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
+                         bmask, bp, bkg);
+            interleave<SCHED, kMfmaPerChunk, kVmemPerChunk>();
+            __syncthreads();
+        }
+        mma((nchunks - 1) & 1);
     }
 
     // epilogue: lane owns pixel (lane & 31) of each 32-wide block
@@ -274,35 +508,60 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     }
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP>
-hipError_t run_conv(const Geom &g, const void *D, const void *W, void *O, hipStream_t st) {
-    using C = Cfg<Tr, WM, WP, FM, FP>;
+template <typename Tr, int WM, int WP, int FM, int FP, int SCHED, bool KVEC>
+hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major) {
+    using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
     using T = typename C::T;
     const int tiles_m = (g.M + C::TM - 1) / C::TM;
     const long long tiles_p = (g.P_total + C::TP - 1) / C::TP;
     const long long total = tiles_p * tiles_m;
     if (total > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    const int kvec = (g.K % C::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0) ? 1 : 0;
-    conv_kernel<Tr, WM, WP, FM, FP><<<(unsigned)total, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D), static_cast<const T *>(W),
-                                                       static_cast<T *>(O), g, tiles_m, (int)total, kvec);
+    auto kern = conv_kernel<Tr, WM, WP, FM, FP, SCHED, KVEC>;
+    if constexpr (C::LDS_BYTES > 65536) {
+        static const hipError_t attr = hipFuncSetAttribute(
+            reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
+        if (attr != hipSuccess) return attr;
+    }
+    kern<<<(unsigned)total, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D), static_cast<const T *>(W),
+                                                       static_cast<T *>(O), g, tiles_m, (int)total, m_major);
     return hipGetLastError();
+}
+
+template <typename Tr, int WM, int WP, int FM, int FP, int SCHED = 0>
+hipError_t run_conv(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major = 0) {
+    const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+    if (kvec) return launch_one<Tr, WM, WP, FM, FP, SCHED, true>(g, D, W, O, st, m_major);
+    return launch_one<Tr, WM, WP, FM, FP, SCHED, false>(g, D, W, O, st, m_major);
 }
 
 }  // namespace
 
-// Tile choice per layer: the filter tile follows M (small-M layers would waste
-// most of a 128-row tile); pixel tiles are as wide as the register budget allows.
+// Tile choice per layer (fp32 rules from a sweep over the workload shapes on
+// MI355X): the filter tile follows M so small-M layers waste no MFMA rows; for
+// larger M the biggest tile that still leaves about two workgroups per CU wins,
+// except that layers with large W (M >= 512, K >= 4096) prefer 256-row tiles,
+// which halve the im2col traffic per flop.
+namespace {
+long long n_tiles(const Geom &g, int tm, int tp) {
+    return ((g.P_total + tp - 1) / tp) * (long long)((g.M + tm - 1) / tm);
+}
+}  // namespace
+
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st) {
     const Geom &g = pl.g;
     if (g.dtype == FTCNN_F32) {
-        if (g.M <= 32) return run_conv<F32T, 1, 4, 1, 2>(g, D, W, O, st);
-        if (g.M <= 64) return run_conv<F32T, 1, 4, 2, 2>(g, D, W, O, st);
-        if (g.M <= 96) return run_conv<F32T, 1, 4, 3, 2>(g, D, W, O, st);
-        return run_conv<F32T, 2, 2, 2, 2>(g, D, W, O, st);
+        if (g.M <= 32) return run_conv<F32T<16>, 1, 4, 1, 2, 4>(g, D, W, O, st);
+        if (g.M <= 64) return run_conv<F32T<16>, 2, 2, 1, 2, 4>(g, D, W, O, st);
+        if (g.M <= 96) return run_conv<F32T<16>, 1, 4, 3, 2, 4>(g, D, W, O, st);
+        if (g.M >= 512 && g.K >= 4096 && n_tiles(g, 256, 128) >= 256)
+            return run_conv<F32T<16>, 4, 2, 2, 2, 4>(g, D, W, O, st);
+        if (n_tiles(g, 128, 128) >= 600) return run_conv<F32T<16>, 2, 2, 2, 2, 4>(g, D, W, O, st);
+        if (n_tiles(g, 128, 64) >= 380) return run_conv<F32T<32>, 2, 2, 2, 1, 4>(g, D, W, O, st);
+        return run_conv<F32T<32>, 2, 2, 1, 1, 4>(g, D, W, O, st);
     }
-    if (g.M <= 32) return run_conv<BF16T, 1, 4, 1, 2>(g, D, W, O, st);
-    if (g.M <= 64) return run_conv<BF16T, 1, 4, 2, 2>(g, D, W, O, st);
-    return run_conv<BF16T, 2, 2, 2, 2>(g, D, W, O, st);
+    if (g.M <= 32) return run_conv<BF16T<32>, 1, 4, 1, 2>(g, D, W, O, st);
+    if (g.M <= 64) return run_conv<BF16T<32>, 1, 4, 2, 2>(g, D, W, O, st);
+    return run_conv<BF16T<32>, 2, 2, 2, 2>(g, D, W, O, st);
 }
 
 }  // namespace ftcnn

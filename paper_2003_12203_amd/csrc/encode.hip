@@ -53,13 +53,14 @@ __global__ __launch_bounds__(kThreads) void encode_partial(const T *__restrict__
 #pragma unroll
     for (int v = 0; v < VEC; ++v) s1[v] = s2[v] = 0.0;
 
+    constexpr int UNR = VEC == 1 ? 16 : 8;  // loads in flight per lane
     long long r = r0;
-    for (; r + 4 <= r1; r += 4) {
-        float x[4][VEC];
+    for (; r + UNR <= r1; r += UNR) {
+        float x[UNR][VEC];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) Vec<T, VEC>::load(X + (r + u) * cols + col, x[u]);
+        for (int u = 0; u < UNR; ++u) Vec<T, VEC>::load(X + (r + u) * cols + col, x[u]);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < UNR; ++u) {
             const double wgt = (double)(r + u + wbase);
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {

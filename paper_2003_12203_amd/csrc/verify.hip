@@ -75,17 +75,19 @@ __global__ __launch_bounds__(kThreads) void verify_partial(const T *__restrict__
         for (int v = 0; v < VEC; ++v) acc[a][v] = 0.0;
 
     if (active) {
+        // row r = n*M + m; rows advance by rpi, so (n, m) advance by (dn, dm) with one carry
+        const int dn = rpi / g.M, dm = rpi - (rpi / g.M) * g.M;
         long long r = r0 + rg;
-        for (; r + 3 * rpi < r1; r += 4 * rpi) {
-            float x[4][VEC];
+        int n = (int)(r / g.M), m = (int)(r - (long long)n * g.M);
+        constexpr int UNR = VEC == 1 ? 16 : 8;  // loads in flight per lane
+        for (; r + (UNR - 1) * rpi < r1; r += UNR * rpi) {
+            float x[UNR][VEC];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) VLoad<T, VEC>::load(O + (r + u * rpi) * g.EF + col, x[u]);
+            for (int u = 0; u < UNR; ++u) VLoad<T, VEC>::load(O + (r + u * rpi) * g.EF + col, x[u]);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const long long ru = r + u * rpi;
-                const long long n = ru / g.M;
+            for (int u = 0; u < UNR; ++u) {
                 const double wn = (double)(n + g.wbase);
-                const double wm = (double)(ru - n * g.M + g.wbase);
+                const double wm = (double)(m + g.wbase);
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
                     const double e = (double)x[u][v];
@@ -94,14 +96,16 @@ __global__ __launch_bounds__(kThreads) void verify_partial(const T *__restrict__
                     acc[2][v] = fma(wn, e, acc[2][v]);
                     acc[3][v] = fma(e, e, acc[3][v]);
                 }
+                n += dn;
+                m += dm;
+                if (m >= g.M) { m -= g.M; ++n; }
             }
         }
         for (; r < r1; r += rpi) {
             float x[VEC];
             VLoad<T, VEC>::load(O + r * g.EF + col, x);
-            const long long n = r / g.M;
             const double wn = (double)(n + g.wbase);
-            const double wm = (double)(r - n * g.M + g.wbase);
+            const double wm = (double)(m + g.wbase);
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
                 const double e = (double)x[v];
@@ -110,6 +114,9 @@ __global__ __launch_bounds__(kThreads) void verify_partial(const T *__restrict__
                 acc[2][v] = fma(wn, e, acc[2][v]);
                 acc[3][v] = fma(e, e, acc[3][v]);
             }
+            n += dn;
+            m += dm;
+            if (m >= g.M) { m -= g.M; ++n; }
         }
     }
     if (rpi > 1) {  // fold the row groups of this block, in row-group order
@@ -135,22 +142,36 @@ __global__ __launch_bounds__(kThreads) void verify_partial(const T *__restrict__
     }
 }
 
+// TPP lanes (a power of two <= 64, aligned inside a wave) share one position:
+// lane j adds splits j, j + TPP, ... in order, then a fixed butterfly combines
+// the lanes.
+template <int TPP>
 __global__ __launch_bounds__(kThreads) void verify_final(Geom g, int splits, const double *__restrict__ part,
                                                          const double *__restrict__ co5, double *so5,
                                                          double *so6, double *so7, double *q5,
                                                          int *__restrict__ flags, double scale,
                                                          ftcnn_report *rep) {
-    const int p = blockIdx.x * kThreads + threadIdx.x;
-    int flag = 0;
+    const int lane = threadIdx.x % TPP;
+    const int p = blockIdx.x * (kThreads / TPP) + threadIdx.x / TPP;
+    double a = 0.0, b = 0.0, c = 0.0, d = 0.0;
     if (p < g.EF) {
-        double a = 0.0, b = 0.0, c = 0.0, d = 0.0;
-        for (int s = 0; s < splits; ++s) {
+        for (int s = lane; s < splits; s += TPP) {
             const double *ps = part + (size_t)s * 4 * g.EF + p;
             a += ps[0];
             b += ps[g.EF];
             c += ps[2 * (size_t)g.EF];
             d += ps[3 * (size_t)g.EF];
         }
+    }
+#pragma unroll
+    for (int o = TPP / 2; o > 0; o >>= 1) {
+        a += __shfl_xor(a, o, 64);
+        b += __shfl_xor(b, o, 64);
+        c += __shfl_xor(c, o, 64);
+        d += __shfl_xor(d, o, 64);
+    }
+    int flag = 0;
+    if (p < g.EF && lane == 0) {
         const double q = sqrt(d);
         so5[p] = a;
         so6[p] = b;
@@ -197,8 +218,16 @@ hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &c
                                   : run<uint16_t, 1>(pl, o, part, rep, cap, st);
     }
     if (e != hipSuccess) return e;
-    verify_final<<<(unsigned)((g.EF + kThreads - 1) / kThreads), kThreads, 0, st>>>(
-        g, pl.ver_splits, part, ck.co5, ck.so5, ck.so6, ck.so7, ck.q5, flags, tol_scale(g, pol.kappa), rep);
+    const double scale = tol_scale(g, pol.kappa);
+    const int sp = pl.ver_splits;
+#define FINAL(TPP)                                                                                     \
+    verify_final<TPP><<<(unsigned)((g.EF + kThreads / TPP - 1) / (kThreads / TPP)), kThreads, 0, st>>>( \
+        g, sp, part, ck.co5, ck.so5, ck.so6, ck.so7, ck.q5, flags, scale, rep)
+    if (sp <= 1) FINAL(1);
+    else if (sp <= 4) FINAL(4);
+    else if (sp <= 16) FINAL(16);
+    else FINAL(64);
+#undef FINAL
     return hipGetLastError();
 }
 
