@@ -97,8 +97,16 @@ def main():
             L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
             if inject and li == i % nl:
                 L.inject(r.O, [r.fault])
-            L.verify(r.O)
-            L.correct(r.D, r.W, r.O)
+            L.verify_correct(r.D, r.W, r.O)
+
+    side = torch.cuda.Stream()
+    done = [torch.cuda.Event() for _ in runs]
+
+    def overlapped_step(i, inject=True):
+        for li, r in enumerate(runs):
+            f = [r.fault] if inject and li == i % nl else ()
+            r.lay.protected_overlapped(r.D, r.W, r.O, side, f, done[li])
+            done[li].record()
 
     def conv_step(ev=None):
         for li, r in enumerate(runs):
@@ -148,9 +156,13 @@ def main():
     # ---- reference loops: error-free protected, unprotected --------------------------
     t_clean = timed(lambda i: protected_step(i, False), args.steps)
     t_unprot = timed(lambda i: conv_step(), args.steps)
+    t_ovl = timed(lambda i: overlapped_step(i, True), args.steps)
+    ovl_rep = runs[(args.steps - 1) % nl].lay.read_report()
+    ovl_ok = ovl_rep.detected and ovl_rep.status == ft.STATUS_CORRECTED
+    t_ovl_clean = timed(lambda i: overlapped_step(i, False), args.steps)
 
     # ---- per-layer stage breakdown (events between the calls) ------------------------
-    stages = ["encode", "conv", "checksum_conv", "verify", "correct"]
+    stages = ["encode", "conv", "checksum_conv", "verify_correct"]
     reps = max(3, min(args.steps, 10))
     stage_ms = np.zeros((reps, nl, len(stages)))
     for k in range(reps):
@@ -165,10 +177,8 @@ def main():
             e[2].record()
             L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
             e[3].record()
-            L.verify(r.O)
+            L.verify_correct(r.D, r.W, r.O)
             e[4].record()
-            L.correct(r.D, r.W, r.O)
-            e[5].record()
         torch.cuda.synchronize()
         for li in range(nl):
             for s in range(len(stages)):
@@ -226,6 +236,12 @@ def main():
         "unprotected_tflops": round(total_flops / t_unprot / 1e12, 3),
         "overhead_error_free_pct": round((t_clean / t_unprot - 1) * 100, 2),
         "overhead_erroneous_pct": round((t_prot / t_unprot - 1) * 100, 2),
+        "overlapped": {"tflops": round(total_flops / t_ovl / 1e12, 3),
+                       "error_free_tflops": round(total_flops / t_ovl_clean / 1e12, 3),
+                       "overhead_erroneous_pct": round((t_ovl / t_unprot - 1) * 100, 2),
+                       "overhead_error_free_pct": round((t_ovl_clean / t_unprot - 1) * 100, 2),
+                       "fault_corrected": bool(ovl_ok),
+                       "note": "encode(D) and Co5-Co7 on a second stream, concurrent with the convolution"},
         "fault_corrected": bool(ok_fault),
         "clean_layers_clean": bool(clean_ok),
         "per_layer": per_layer,

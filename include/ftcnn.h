@@ -103,9 +103,10 @@ enum {
 
 typedef struct { int32_t n, m, x, y, scheme; } ftcnn_fix;
 
-/* Detection and correction report, in device (or device-visible host) memory.
- * ftcnn_verify() resets it; ftcnn_correct() fills in the repairs.  fixes[] is
- * in no particular order; n_fixes counts every repair even past cap_fixes. */
+/* Detection and correction report, in device memory (updated with device
+ * atomics).  ftcnn_verify() resets it; ftcnn_correct() fills in the repairs.
+ * fixes[] is in no particular order; n_fixes counts every repair even past
+ * cap_fixes. */
 typedef struct {
     int32_t detected;          /* CoC-D verdict for the layer                     */
     int32_t n_flagged;         /* positions p with Co5 - So5 beyond tolerance     */
@@ -191,8 +192,16 @@ int ftcnn_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, voi
                   const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                   void *workspace, hipStream_t stream);
 
-/* The whole error-free path of one protected layer on one stream:
- * encode(D) -> conv_fwd -> checksum_conv(CO5|CO6|CO7) -> verify -> correct.
+/* ftcnn_verify and ftcnn_correct in two launches: the final detection stage
+ * runs the correction chain of ftcnn_correct in the same workgroup for every
+ * position it flags, so a clean layer pays nothing for the correction module.
+ * Same inputs, outputs and report as the two calls in sequence. */
+int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                         const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                         int32_t cap_fixes, void *workspace, hipStream_t stream);
+
+/* The whole path of one protected layer on one stream:
+ * encode(D) -> conv_fwd -> checksum_conv(CO5|CO6|CO7) -> verify_correct.
  * ck->cw1/cw2 must hold the encoded W (ftcnn_encode with which = 1). */
 int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                          const ftcnn_checksums *ck, const ftcnn_policy *policy,

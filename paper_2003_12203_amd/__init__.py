@@ -107,6 +107,12 @@ def correct(desc, D, W, O, ck, policy, report, workspace, stream=None) -> None:
                                _ptr(report), _ptr(workspace), _stream(stream)), "ftcnn_correct")
 
 
+def verify_correct(desc, D, W, O, ck, policy, report, cap, workspace, stream=None) -> None:
+    _check(lib().ftcnn_verify_correct(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck), C.byref(policy),
+                                      _ptr(report), cap, _ptr(workspace), _stream(stream)),
+           "ftcnn_verify_correct")
+
+
 def protected_conv(desc, D, W, O, ck, policy, report, cap, workspace, stream=None) -> None:
     _check(lib().ftcnn_protected_conv(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck),
                                       C.byref(policy), _ptr(report), cap, _ptr(workspace),
@@ -219,6 +225,9 @@ class Layer:
     def correct(self, D, W, O, stream=None):
         correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.workspace, stream)
 
+    def verify_correct(self, D, W, O, stream=None):
+        verify_correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace, stream)
+
     def protected(self, D, W, O, stream=None):
         protected_conv(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace,
                        stream)
@@ -229,6 +238,29 @@ class Layer:
     def read_report(self) -> Report:
         torch.cuda.synchronize()
         return parse_report(self.report)
+
+    def protected_overlapped(self, D, W, O, side, faults=(), done=None):
+        """The protected layer with the input checksums on a second stream.
+
+        encode(D) and checksum_conv(Co5, Co6, Co7) need only D and the weight
+        checksums, so they run on ``side`` while the convolution runs on the
+        current stream; verify_correct waits for both.  ``done`` (an event the
+        caller records after the previous use of this layer) keeps the next
+        encode from overwriting checksums a pending correction still reads.
+        """
+        main = torch.cuda.current_stream()
+        ready = torch.cuda.Event()
+        with torch.cuda.stream(side):
+            if done is not None:
+                side.wait_event(done)
+            self.encode_input(D, side)
+            self.checksum_conv(CO5 | CO6 | CO7, stream=side)
+            ready.record(side)
+        self.conv(D, W, O, main)
+        if faults:
+            self.inject(O, faults, main)
+        main.wait_event(ready)
+        self.verify_correct(D, W, O, main)
 
     def run(self, D, W, O, faults=(), stream=None) -> Report:
         """The full workflow of Sec. 4.3 with recomputation of the layer when needed (Sec. 4.1.1)."""

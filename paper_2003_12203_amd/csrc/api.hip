@@ -83,6 +83,11 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     if (pl->ver_splits > part_cap) pl->ver_splits = part_cap > 1 ? (int)part_cap : 1;
     // correction
     pl->corr_blocks = 256;
+    {
+        const int per = kThreads / final_tpp(pl->ver_splits);
+        const long long fblocks = ceil_div(EF, per);
+        pl->corr_slots = (int)(fblocks > pl->corr_blocks ? fblocks : pl->corr_blocks);
+    }
     const long long L = g.M > g.N ? g.M : g.N;
     pl->corr_stride = (size_t)((4LL * g.M + 4LL * g.N + 2 * L + 31) / 32 * 32);
 
@@ -96,7 +101,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     pl->off_ver = off;
     off += align256(4ull * pl->ver_splits * EF * sizeof(double));
     pl->off_corr = off;
-    off += align256((size_t)pl->corr_blocks * pl->corr_stride * sizeof(double));
+    off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
     pl->bytes = off;
     return FTCNN_OK;
 }
@@ -175,6 +180,20 @@ int do_verify(const Plan &pl, const void *O, const ftcnn_checksums *ck, const ft
     if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
     FT_TRY(check_ws(pl, ws));
     FT_HIP(launch_verify(pl, O, *ck, *pol, rep, cap, ws, st), "verify");
+    return FTCNN_OK;
+}
+
+int do_verify_correct(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
+                      const ftcnn_policy *pol, ftcnn_report *rep, int32_t cap, void *ws, hipStream_t st) {
+    FT_TRY(check_policy(pol));
+    if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "verify_correct: null pointer");
+    if (!ck->co5 || !ck->so5 || !ck->so6 || !ck->so7 || !ck->q5)
+        return fail(FTCNN_E_ARG, "verify needs co5, so5, so6, so7 and q5");
+    if (!ck->cd1 || !ck->cd2 || !ck->cw1 || !ck->cw2 || !ck->co6 || !ck->co7)
+        return fail(FTCNN_E_ARG, "correct needs cd1, cd2, cw1, cw2, co5, co6 and co7");
+    if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
+    FT_TRY(check_ws(pl, ws));
+    FT_HIP(launch_verify_correct(pl, D, W, O, *ck, *pol, rep, cap, ws, st), "verify_correct");
     return FTCNN_OK;
 }
 
@@ -263,8 +282,15 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
     FT_TRY(do_encode(pl, 0, D, ck->cd1, ck->cd2, workspace, stream));
     FT_TRY(do_conv(pl, D, W, O, stream));
     FT_TRY(do_cksum(pl, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, D, W, ck, stream));
-    FT_TRY(do_verify(pl, O, ck, policy, rep, cap_fixes, workspace, stream));
-    return do_correct(pl, D, W, O, ck, policy, rep, workspace, stream);
+    return do_verify_correct(pl, D, W, O, ck, policy, rep, cap_fixes, workspace, stream);
+}
+
+int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                         const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                         int32_t cap_fixes, void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_verify_correct(pl, D, W, O, ck, policy, rep, cap_fixes, workspace, stream);
 }
 
 int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults, int32_t nf,

@@ -540,13 +540,9 @@ template <typename T> __device__ void resolve(const Ctx<T> &c, Sh &sh, int p) {
     record(c, sh, FTCNN_SCHEME_UNRESOLVED, x, y);
 }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void correct_kernel(Ctx<T> c, const int *__restrict__ flags,
-                                                           double *scratch, size_t stride, int chunk) {
-    if (c.rep->detected == 0) return;
-    __shared__ Sh sh;
+// Point the per-position arrays of c at this workgroup's slice of scratch.
+template <typename T> __device__ inline void bind_scratch(Ctx<T> &c, double *mine) {
     const Geom &g = c.g;
-    double *mine = scratch + stride * blockIdx.x;
     const int L = g.M > g.N ? g.M : g.N;
     c.co1m = mine;
     c.d1 = c.co1m + g.M;
@@ -559,6 +555,15 @@ __global__ __launch_bounds__(kThreads) void correct_kernel(Ctx<T> c, const int *
     c.fix_old = reinterpret_cast<uint32_t *>(c.q2 + g.N);
     c.fix_n = reinterpret_cast<int *>(c.fix_old + L);
     c.fix_m = c.fix_n + L;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void correct_kernel(Ctx<T> c, const int *__restrict__ flags,
+                                                           double *scratch, size_t stride, int chunk) {
+    if (c.rep->detected == 0) return;
+    __shared__ Sh sh;
+    const Geom &g = c.g;
+    bind_scratch(c, scratch + stride * blockIdx.x);
     // positions are dealt in chunks of `chunk` (<= kThreads) so that flagged
     // positions of small layers still spread over many workgroups
     for (int base = blockIdx.x * chunk; base < g.EF; base += gridDim.x * chunk) {
@@ -576,6 +581,106 @@ __global__ __launch_bounds__(kThreads) void correct_kernel(Ctx<T> c, const int *
         for (int i = 0; i < cnt; ++i) resolve(c, sh, sh.list[i]);
         __syncthreads();
     }
+}
+
+// Final stage of the detection (the split partials of each position summed in a
+// fixed order, then the CoC-D test) with the correction chain run in the same
+// workgroup for every position it flags.  A clean layer pays nothing for the
+// correction module, and no separate launch is needed.
+template <typename T, int TPP>
+__global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int splits, const double *__restrict__ part,
+                                                                  double *so5, double *so6, double *so7, double *q5,
+                                                                  int *__restrict__ flags, double *scratch,
+                                                                  size_t stride) {
+    __shared__ Sh sh;
+    const Geom &g = c.g;
+    const int per = kThreads / TPP;
+    const int lane = threadIdx.x % TPP, slot = threadIdx.x / TPP;
+    const int p = blockIdx.x * per + slot;
+    double a = 0.0, b = 0.0, cc = 0.0, d = 0.0;
+    if (p < g.EF) {
+        for (int s = lane; s < splits; s += TPP) {
+            const double *ps = part + (size_t)s * 4 * g.EF + p;
+            a += ps[0];
+            b += ps[g.EF];
+            cc += ps[2 * (size_t)g.EF];
+            d += ps[3 * (size_t)g.EF];
+        }
+    }
+#pragma unroll
+    for (int o = TPP / 2; o > 0; o >>= 1) {
+        a += __shfl_xor(a, o, 64);
+        b += __shfl_xor(b, o, 64);
+        cc += __shfl_xor(cc, o, 64);
+        d += __shfl_xor(d, o, 64);
+    }
+    int flag = 0;
+    if (p < g.EF && lane == 0) {
+        const double q = sqrt(d);
+        so5[p] = a;
+        so6[p] = b;
+        so7[p] = cc;
+        q5[p] = q;
+        flag = is_bad(c.co5g[p] - a, q, c.scale) ? 1 : 0;
+        flags[p] = flag;
+        sh.flagbuf[slot] = flag;
+    }
+    const int cnt = __syncthreads_count(flag);
+    if (cnt == 0) return;
+    if (threadIdx.x == 0) {
+        atomicAdd(&c.rep->n_flagged, cnt);
+        atomicMax(&c.rep->detected, 1);
+        int n = 0;
+        for (int t = 0; t < per; ++t)
+            if (blockIdx.x * per + t < g.EF && sh.flagbuf[t]) sh.list[n++] = blockIdx.x * per + t;
+        sh.nlist = n;
+    }
+    __syncthreads();
+    bind_scratch(c, scratch + stride * blockIdx.x);
+    const int nl = sh.nlist;
+    for (int i = 0; i < nl; ++i) resolve(c, sh, sh.list[i]);
+}
+
+template <typename T>
+Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums &ck,
+                const ftcnn_policy &pol, ftcnn_report *rep) {
+    Ctx<T> c{};
+    c.g = pl.g;
+    c.D = static_cast<const T *>(D);
+    c.W = static_cast<const T *>(W);
+    c.O = static_cast<T *>(O);
+    c.cd1 = ck.cd1; c.cd2 = ck.cd2; c.cw1 = ck.cw1; c.cw2 = ck.cw2;
+    c.co5g = ck.co5; c.co6g = ck.co6; c.co7g = ck.co7;
+    c.scale = tol_scale(pl.g, pol.kappa);
+    c.eta = pol.eta;
+    c.wb = pl.g.wbase;
+    c.rc_on = pol.rc_on;
+    c.clc_on = pol.clc_on;
+    c.recompute = pol.repair == FTCNN_REPAIR_RECOMPUTE;
+    c.rep = rep;
+    return c;
+}
+
+template <typename T>
+hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums &ck,
+                     const ftcnn_policy &pol, ftcnn_report *rep, void *ws, hipStream_t st) {
+    const Ctx<T> c = make_ctx<T>(pl, D, W, O, ck, pol, rep);
+    char *w = static_cast<char *>(ws);
+    const double *part = reinterpret_cast<const double *>(w + pl.off_ver);
+    int *flags = reinterpret_cast<int *>(w + pl.off_flags);
+    double *scratch = reinterpret_cast<double *>(w + pl.off_corr);
+    const int sp = pl.ver_splits;
+    const int tpp = final_tpp(sp);
+    const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
+#define VC(TPP)                                                                                          \
+    verify_correct_kernel<T, TPP><<<blocks, kThreads, 0, st>>>(c, sp, part, ck.so5, ck.so6, ck.so7, ck.q5, \
+                                                               flags, scratch, pl.corr_stride)
+    if (tpp == 1) VC(1);
+    else if (tpp == 4) VC(4);
+    else if (tpp == 16) VC(16);
+    else VC(64);
+#undef VC
+    return hipGetLastError();
 }
 
 template <typename T>
@@ -611,6 +716,15 @@ hipError_t launch_correct(const Plan &pl, const void *D, const void *W, void *O,
                           void *ws, hipStream_t st) {
     if (pl.g.dtype == FTCNN_F32) return run<float>(pl, D, W, O, ck, pol, rep, ws, st);
     return run<uint16_t>(pl, D, W, O, ck, pol, rep, ws, st);
+}
+
+hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, void *O,
+                                 const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
+                                 int cap, void *ws, hipStream_t st) {
+    hipError_t e = launch_verify_partial(pl, O, rep, cap, ws, st);
+    if (e != hipSuccess) return e;
+    if (pl.g.dtype == FTCNN_F32) return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, st);
 }
 
 }  // namespace ftcnn

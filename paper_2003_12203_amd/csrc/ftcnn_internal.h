@@ -30,6 +30,7 @@ struct Plan {
     int ver_splits;                   // row splits of the verification reduction
     int ver_cols_per_block;           // columns handled by one verify block
     int corr_blocks;                  // workgroups of the correction kernel
+    int corr_slots;                   // per-workgroup scratch slices (correction or fused verification)
     size_t off_flags, off_enc, off_ver, off_corr, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
@@ -86,6 +87,15 @@ hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &c
 hipError_t launch_correct(const Plan &pl, const void *D, const void *W, void *O,
                           const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
                           void *ws, hipStream_t st);
+hipError_t launch_verify_partial(const Plan &pl, const void *O, ftcnn_report *rep, int cap, void *ws,
+                                 hipStream_t st);
+hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, void *O,
+                                 const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
+                                 int cap, void *ws, hipStream_t st);
+
+// Threads that share one position in the final verification stage (a power of
+// two; the float64 split partials of that position are spread over them).
+inline int final_tpp(int splits) { return splits <= 1 ? 1 : splits <= 4 ? 4 : splits <= 16 ? 16 : 64; }
 hipError_t launch_inject(const Plan &pl, void *O, const ftcnn_fault *f, int nf, hipStream_t st);
 
 }  // namespace ftcnn

@@ -188,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void verify_final(Geom g, int splits, con
 }
 
 template <typename T, int VEC>
-hipError_t run(const Plan &pl, const T *O, double *part, ftcnn_report *rep, int cap, hipStream_t st) {
+hipError_t run_partial(const Plan &pl, const T *O, double *part, ftcnn_report *rep, int cap, hipStream_t st) {
     const Geom &g = pl.g;
     const int cols_v = (g.EF + VEC - 1) / VEC;
     const int ctt = cols_v < kThreads ? cols_v : kThreads;
@@ -200,6 +200,21 @@ hipError_t run(const Plan &pl, const T *O, double *part, ftcnn_report *rep, int 
 
 }  // namespace
 
+hipError_t launch_verify_partial(const Plan &pl, const void *O, ftcnn_report *rep, int cap, void *ws,
+                                 hipStream_t st) {
+    const Geom &g = pl.g;
+    double *part = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_ver);
+    const bool al = reinterpret_cast<uintptr_t>(O) % 16 == 0;
+    if (g.dtype == FTCNN_F32) {
+        const float *o = static_cast<const float *>(O);
+        return (g.EF % 4 == 0 && al) ? run_partial<float, 4>(pl, o, part, rep, cap, st)
+                                     : run_partial<float, 1>(pl, o, part, rep, cap, st);
+    }
+    const uint16_t *o = static_cast<const uint16_t *>(O);
+    return (g.EF % 8 == 0 && al) ? run_partial<uint16_t, 8>(pl, o, part, rep, cap, st)
+                                 : run_partial<uint16_t, 1>(pl, o, part, rep, cap, st);
+}
+
 hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &ck,
                          const ftcnn_policy &pol, ftcnn_report *rep, int cap, void *ws,
                          hipStream_t st) {
@@ -207,16 +222,7 @@ hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &c
     char *w = static_cast<char *>(ws);
     double *part = reinterpret_cast<double *>(w + pl.off_ver);
     int *flags = reinterpret_cast<int *>(w + pl.off_flags);
-    const bool al = reinterpret_cast<uintptr_t>(O) % 16 == 0;
-    hipError_t e;
-    if (g.dtype == FTCNN_F32) {
-        const float *o = static_cast<const float *>(O);
-        e = (g.EF % 4 == 0 && al) ? run<float, 4>(pl, o, part, rep, cap, st) : run<float, 1>(pl, o, part, rep, cap, st);
-    } else {
-        const uint16_t *o = static_cast<const uint16_t *>(O);
-        e = (g.EF % 8 == 0 && al) ? run<uint16_t, 8>(pl, o, part, rep, cap, st)
-                                  : run<uint16_t, 1>(pl, o, part, rep, cap, st);
-    }
+    hipError_t e = launch_verify_partial(pl, O, rep, cap, ws, st);
     if (e != hipSuccess) return e;
     const double scale = tol_scale(g, pol.kappa);
     const int sp = pl.ver_splits;
