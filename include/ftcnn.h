@@ -132,6 +132,12 @@ typedef struct {
     double kappa, eta;         /* defaults 16 and 0.1                             */
 } ftcnn_policy;
 
+/* A fault planted for testing (the paper's source-level injection, Sec. 6.1)
+ * at output element (n, m, x, y): kind 0 flips bit `bit` of the stored fp32 or
+ * bf16 pattern, kind 1 adds `value`, kind 2 stores `value` (both rounded to
+ * the dtype). */
+typedef struct { int32_t n, m, x, y, kind, bit; double value; } ftcnn_fault;
+
 /* ---- host-only queries -------------------------------------------------- */
 
 /* E and F of eq. (1) with zero padding.  Returns FTCNN_E_SHAPE when either is < 1. */
@@ -200,8 +206,31 @@ int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void 
                          const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                          int32_t cap_fixes, void *workspace, hipStream_t stream);
 
+/* Eq. (1) as ftcnn_conv_fwd (same kernel, bitwise the same O), with the
+ * CoC-D summations of Sec. 3.6 computed in the epilogue from the values as
+ * stored: every workgroup tile writes, for each of its output pixels, the
+ * partial So5, So6, So7 and sum of squares over its filters into the
+ * workspace, so detection never re-reads O.  Also resets *rep (cap_fixes
+ * recorded).  Follow it with ftcnn_verify_correct_sums on the same workspace
+ * and report.
+ * faults / nf: TEST ONLY, NULL / 0 otherwise.  A HOST array of at most 64
+ * faults planted in the output values before they are summed and stored, as
+ * a fault of the convolution's own arithmetic would appear (Sec. 6.1).
+ * Checks every fault as ftcnn_inject does. */
+int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                        ftcnn_report *rep, int32_t cap_fixes, const ftcnn_fault *faults, int32_t nf,
+                        void *workspace, hipStream_t stream);
+
+/* ftcnn_verify_correct over the partial sums that ftcnn_conv_fwd_sums left in
+ * the workspace (one launch; O is read only at flagged positions).  The
+ * report must be the one ftcnn_conv_fwd_sums reset.  Writes ck->so5, so6,
+ * so7, q5 and the flag map; same decisions and repairs as ftcnn_verify_correct. */
+int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                              const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                              void *workspace, hipStream_t stream);
+
 /* The whole path of one protected layer on one stream:
- * encode(D) -> conv_fwd -> checksum_conv(CO5|CO6|CO7) -> verify_correct.
+ * encode(D) -> conv_fwd_sums -> checksum_conv(CO5|CO6|CO7) -> verify_correct_sums.
  * ck->cw1/cw2 must hold the encoded W (ftcnn_encode with which = 1). */
 int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                          const ftcnn_checksums *ck, const ftcnn_policy *policy,
@@ -209,10 +238,8 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
                          hipStream_t stream);
 
 /* TEST ONLY: corrupt stored outputs, reproducing the paper's source-level
- * fault injection (Sec. 6.1).  faults is a HOST array of at most 64 entries:
- * kind 0 flips bit `bit` of the stored pattern, kind 1 adds `value`, kind 2
- * stores `value` (all rounded to the dtype).  Positions must be in range. */
-typedef struct { int32_t n, m, x, y, kind, bit; double value; } ftcnn_fault;
+ * fault injection (Sec. 6.1).  faults is a HOST array of at most 64 entries
+ * (ftcnn_fault above), applied in order.  Positions must be in range. */
 int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults, int32_t nf,
                  hipStream_t stream);
 

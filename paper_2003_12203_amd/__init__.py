@@ -113,19 +113,37 @@ def verify_correct(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
            "ftcnn_verify_correct")
 
 
+def conv_fwd_sums(desc, D, W, O, report, cap, workspace, faults: Sequence[dict] = (), stream=None) -> None:
+    arr = _fault_array(faults)
+    _check(lib().ftcnn_conv_fwd_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), _ptr(report), cap,
+                                     arr if faults else None, len(faults), _ptr(workspace), _stream(stream)),
+           "ftcnn_conv_fwd_sums")
+
+
+def verify_correct_sums(desc, D, W, O, ck, policy, report, workspace, stream=None) -> None:
+    _check(lib().ftcnn_verify_correct_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck),
+                                           C.byref(policy), _ptr(report), _ptr(workspace), _stream(stream)),
+           "ftcnn_verify_correct_sums")
+
+
 def protected_conv(desc, D, W, O, ck, policy, report, cap, workspace, stream=None) -> None:
     _check(lib().ftcnn_protected_conv(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck),
                                       C.byref(policy), _ptr(report), cap, _ptr(workspace),
                                       _stream(stream)), "ftcnn_protected_conv")
 
 
-def inject(desc, O, faults: Sequence[dict], stream=None) -> None:
+def _fault_array(faults: Sequence[dict]):
     arr = (_lib.Fault * max(1, len(faults)))()
     kinds = {"flip": 0, "add": 1, "set": 2}
     for i, f in enumerate(faults):
         arr[i] = _lib.Fault(f["n"], f["m"], f["x"], f["y"], kinds[f["kind"]], f.get("bit", 0),
                             float(f.get("value", 0.0)))
-    _check(lib().ftcnn_inject(C.byref(desc), _ptr(O), arr, len(faults), _stream(stream)), "ftcnn_inject")
+    return arr
+
+
+def inject(desc, O, faults: Sequence[dict], stream=None) -> None:
+    _check(lib().ftcnn_inject(C.byref(desc), _ptr(O), _fault_array(faults), len(faults), _stream(stream)),
+           "ftcnn_inject")
 
 
 # ---- report ----------------------------------------------------------------------
@@ -228,6 +246,12 @@ class Layer:
     def verify_correct(self, D, W, O, stream=None):
         verify_correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace, stream)
 
+    def conv_sums(self, D, W, O, faults=(), stream=None):
+        conv_fwd_sums(self.desc, D, W, O, self.report, self.cap, self.workspace, faults, stream)
+
+    def verify_correct_sums(self, D, W, O, stream=None):
+        verify_correct_sums(self.desc, D, W, O, self.ck, self.policy, self.report, self.workspace, stream)
+
     def protected(self, D, W, O, stream=None):
         protected_conv(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace,
                        stream)
@@ -239,14 +263,26 @@ class Layer:
         torch.cuda.synchronize()
         return parse_report(self.report)
 
-    def protected_overlapped(self, D, W, O, side, faults=(), done=None):
+    def protected_fused(self, D, W, O, faults=(), stream=None):
+        """The protected layer on one stream with the summations in the convolution's epilogue:
+        encode(D) -> conv_fwd_sums -> checksum_conv(Co5, Co6, Co7) -> verify_correct_sums.
+        ``faults`` (testing) are planted in the convolution's outputs before they are summed."""
+        self.encode_input(D, stream)
+        self.conv_sums(D, W, O, faults, stream)
+        self.checksum_conv(CO5 | CO6 | CO7, stream=stream)
+        self.verify_correct_sums(D, W, O, stream)
+
+    def protected_overlapped(self, D, W, O, side, faults=(), done=None, fused=True):
         """The protected layer with the input checksums on a second stream.
 
         encode(D) and checksum_conv(Co5, Co6, Co7) need only D and the weight
         checksums, so they run on ``side`` while the convolution runs on the
-        current stream; verify_correct waits for both.  ``done`` (an event the
-        caller records after the previous use of this layer) keeps the next
-        encode from overwriting checksums a pending correction still reads.
+        current stream; the final detection and correction wait for both.
+        ``done`` (an event the caller records after the previous use of this
+        layer) keeps the next encode from overwriting checksums a pending
+        correction still reads.  fused=True sums O in the convolution's
+        epilogue (faults are planted there); otherwise O is re-read by
+        verify_correct after ``faults`` are injected into it.
         """
         main = torch.cuda.current_stream()
         ready = torch.cuda.Event()
@@ -256,6 +292,11 @@ class Layer:
             self.encode_input(D, side)
             self.checksum_conv(CO5 | CO6 | CO7, stream=side)
             ready.record(side)
+        if fused:
+            self.conv_sums(D, W, O, faults, main)
+            main.wait_event(ready)
+            self.verify_correct_sums(D, W, O, main)
+            return
         self.conv(D, W, O, main)
         if faults:
             self.inject(O, faults, main)

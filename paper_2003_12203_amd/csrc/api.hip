@@ -81,11 +81,14 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     const long long part_cap = part_budget / (32 * EF);
     pl->ver_splits = row_splits(rows_o, ceil_div(cols_v, ctt), 1024, 32);
     if (pl->ver_splits > part_cap) pl->ver_splits = part_cap > 1 ? (int)part_cap : 1;
-    // correction
+    // summations fused into the convolution epilogue: one slice per (filter tile, image)
+    pl->sum_splits = (int)(ceil_div(g.M, conv_tile_m(g)) * g.N);
+    // correction: one scratch slice per workgroup of the widest final detection stage
     pl->corr_blocks = 256;
     {
-        const int per = kThreads / final_tpp(pl->ver_splits);
-        const long long fblocks = ceil_div(EF, per);
+        const int tpp = final_tpp(pl->ver_splits) < final_tpp(pl->sum_splits) ? final_tpp(pl->ver_splits)
+                                                                               : final_tpp(pl->sum_splits);
+        const long long fblocks = ceil_div(EF, kThreads / tpp);
         pl->corr_slots = (int)(fblocks > pl->corr_blocks ? fblocks : pl->corr_blocks);
     }
     const long long L = g.M > g.N ? g.M : g.N;
@@ -100,6 +103,8 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     off += align256(enc_d > enc_w ? enc_d : enc_w);
     pl->off_ver = off;
     off += align256(4ull * pl->ver_splits * EF * sizeof(double));
+    pl->off_sums = off;
+    off += align256(4ull * pl->sum_splits * EF * sizeof(double));
     pl->off_corr = off;
     off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
     pl->bytes = off;
@@ -197,6 +202,43 @@ int do_verify_correct(const Plan &pl, const void *D, const void *W, void *O, con
     return FTCNN_OK;
 }
 
+int check_faults(const Geom &g, const ftcnn_fault *faults, int nf, const char *who) {
+    if (nf > 0 && !faults) return fail(FTCNN_E_ARG, "%s: null fault list", who);
+    if (nf < 0 || nf > kMaxFaults) return fail(FTCNN_E_ARG, "%s: %d faults (at most %d)", who, nf, kMaxFaults);
+    const int bits = g.dtype == FTCNN_F32 ? 32 : 16;
+    for (int i = 0; i < nf; ++i) {
+        const ftcnn_fault &f = faults[i];
+        if (f.n < 0 || f.n >= g.N || f.m < 0 || f.m >= g.M || f.x < 0 || f.x >= g.E || f.y < 0 || f.y >= g.F)
+            return fail(FTCNN_E_ARG, "%s: fault %d out of range", who, i);
+        if (f.kind < 0 || f.kind > 2 || (f.kind == 0 && (f.bit < 0 || f.bit >= bits)))
+            return fail(FTCNN_E_ARG, "%s: fault %d has kind %d bit %d", who, i, f.kind, f.bit);
+    }
+    return FTCNN_OK;
+}
+
+int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, ftcnn_report *rep, int32_t cap,
+                 const ftcnn_fault *faults, int32_t nf, void *ws, hipStream_t st) {
+    if (!D || !W || !O || !rep) return fail(FTCNN_E_ARG, "conv_fwd_sums: null pointer");
+    if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
+    FT_TRY(check_faults(pl.g, faults, nf, "conv_fwd_sums"));
+    FT_TRY(check_ws(pl, ws));
+    FT_HIP(launch_conv_sums(pl, D, W, O, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
+    return FTCNN_OK;
+}
+
+int do_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
+                           const ftcnn_policy *pol, ftcnn_report *rep, void *ws, hipStream_t st) {
+    FT_TRY(check_policy(pol));
+    if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "verify_correct_sums: null pointer");
+    if (!ck->co5 || !ck->so5 || !ck->so6 || !ck->so7 || !ck->q5)
+        return fail(FTCNN_E_ARG, "verify needs co5, so5, so6, so7 and q5");
+    if (!ck->cd1 || !ck->cd2 || !ck->cw1 || !ck->cw2 || !ck->co6 || !ck->co7)
+        return fail(FTCNN_E_ARG, "correct needs cd1, cd2, cw1, cw2, co5, co6 and co7");
+    FT_TRY(check_ws(pl, ws));
+    FT_HIP(launch_verify_correct_sums(pl, D, W, O, *ck, *pol, rep, ws, st), "verify_correct_sums");
+    return FTCNN_OK;
+}
+
 int do_correct(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
                const ftcnn_policy *pol, ftcnn_report *rep, void *ws, hipStream_t st) {
     FT_TRY(check_policy(pol));
@@ -280,9 +322,25 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
     if (!ck || !D || !W || !O || !rep) return fail(FTCNN_E_ARG, "protected_conv: null pointer");
     FT_TRY(check_ws(pl, workspace));
     FT_TRY(do_encode(pl, 0, D, ck->cd1, ck->cd2, workspace, stream));
-    FT_TRY(do_conv(pl, D, W, O, stream));
+    FT_TRY(do_conv_sums(pl, D, W, O, rep, cap_fixes, nullptr, 0, workspace, stream));
     FT_TRY(do_cksum(pl, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, D, W, ck, stream));
-    return do_verify_correct(pl, D, W, O, ck, policy, rep, cap_fixes, workspace, stream);
+    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, workspace, stream);
+}
+
+int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O, ftcnn_report *rep,
+                        int32_t cap_fixes, const ftcnn_fault *faults, int32_t nf, void *workspace,
+                        hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_conv_sums(pl, D, W, O, rep, cap_fixes, faults, nf, workspace, stream);
+}
+
+int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                              const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                              void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, workspace, stream);
 }
 
 int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
@@ -297,17 +355,8 @@ int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults
                  hipStream_t stream) {
     Plan pl;
     FT_TRY(make_plan(desc, &pl));
-    if (!O || (nf > 0 && !faults)) return fail(FTCNN_E_ARG, "inject: null pointer");
-    if (nf < 0 || nf > kMaxFaults) return fail(FTCNN_E_ARG, "inject: %d faults (at most %d)", nf, kMaxFaults);
-    const Geom &g = pl.g;
-    const int bits = g.dtype == FTCNN_F32 ? 32 : 16;
-    for (int i = 0; i < nf; ++i) {
-        const ftcnn_fault &f = faults[i];
-        if (f.n < 0 || f.n >= g.N || f.m < 0 || f.m >= g.M || f.x < 0 || f.x >= g.E || f.y < 0 || f.y >= g.F)
-            return fail(FTCNN_E_ARG, "inject: fault %d out of range", i);
-        if (f.kind < 0 || f.kind > 2 || (f.kind == 0 && (f.bit < 0 || f.bit >= bits)))
-            return fail(FTCNN_E_ARG, "inject: fault %d has kind %d bit %d", i, f.kind, f.bit);
-    }
+    if (!O) return fail(FTCNN_E_ARG, "inject: null pointer");
+    FT_TRY(check_faults(pl.g, faults, nf, "inject"));
     if (nf == 0) return FTCNN_OK;
     FT_HIP(launch_inject(pl, O, faults, nf, stream), "inject");
     return FTCNN_OK;

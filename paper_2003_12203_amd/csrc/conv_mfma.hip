@@ -14,6 +14,8 @@
 // so the epilogue writes whole 128-byte runs of O.  Workgroup ids are remapped so
 // that the M tiles of one pixel tile land on the same XCD (its L2 then serves the
 // repeated im2col reads of D).
+#include <type_traits>
+
 #include "ftcnn_internal.h"
 
 namespace ftcnn {
@@ -320,45 +322,38 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
     }
 }
 
-// Instruction interleave for one K chunk: the next chunk's gather (VALU, SALU
-// and VMEM) is spread between this chunk's MFMAs, so the vector ALU and the
-// memory pipeline work while the matrix core is busy.
-template <int SCHED, int NMFMA, int NVMEM>
-__device__ inline void interleave() {
-    if constexpr (SCHED == 1) {
-#pragma unroll
-        for (int i = 0; i < NMFMA; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
-            if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
-            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);      // VALU
-            __builtin_amdgcn_sched_group_barrier(0x004, 2, 0);      // SALU
-        }
-    } else if constexpr (SCHED == 2) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);          // first LDS operand reads
-#pragma unroll
-        for (int i = 0; i < NMFMA; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if (i < 4) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
-            __builtin_amdgcn_sched_group_barrier(0x004, 3, 0);
-        }
-    } else if constexpr (SCHED == 3) {
-#pragma unroll
-        for (int i = 0; i < NMFMA; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if (i % 2 == 0 && i / 2 < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x004, 1, 0);
-        }
-    }
-}
+// Epilogue arguments.  EPI 0: plain store.  EPI 1: the CoC-D summations of
+// every stored value as well (Sec. 3.6): for each pixel p of the tile, the tile's
+// rows give sum O, sum (m + wbase) O, (n + wbase) sum O and sum O^2, written as
+// slice (tile_m * N + n) of a [slices][4][E*F] float64 array; block 0 resets the
+// report.  EPI 2: EPI 1 with faults planted in the stored values first.
+struct NoFaults {};
+template <int EPI> struct Epi {
+    double *part;
+    ftcnn_report *rep;
+    int cap;
+    typename std::conditional<EPI == 2, FaultList, NoFaults>::type fl;
+};
+template <> struct Epi<0> {};
 
-template <typename Tr, int WM, int WP, int FM, int FP, int SCHED = 0, bool KVEC = true>
+template <typename T> struct Bits;
+template <> struct Bits<float> {
+    using B = float;   // an fp32 output is stored as computed
+    __device__ static B make(float v) { return v; }
+    __device__ static float value(B b) { return b; }
+};
+template <> struct Bits<uint16_t> {
+    using B = uint16_t;
+    __device__ static B make(float v) { return f32_to_bf16_bits(v); }
+    __device__ static float value(B b) { return bf16_bits_to_f32(b); }
+};
+
+template <typename Tr, int WM, int WP, int FM, int FP, bool WEAVE, bool KVEC, int EPI>
 __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T *__restrict__ D,
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
-                                                            int tiles_m, int tiles_total, int m_major) {
+                                                            int tiles_m, int tiles_total, int m_major,
+                                                            Epi<EPI> ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
     using T = typename C::T;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -411,20 +406,8 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     __syncthreads();
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    auto mma = [&](int buf) {
-        const T *As = As0 + buf * C::TM * C::LDK;
-        const T *Bs = Bs0 + buf * C::TP * C::LDK;
-        if constexpr (sizeof(T) == 4)
-            mma_f32<C::TK, FM, FP>(reinterpret_cast<const float *>(As), reinterpret_cast<const float *>(Bs),
-                                   lane, arow0, brow0, acc);
-        else
-            mma_bf16<C::TK, FM, FP>(reinterpret_cast<const uint16_t *>(As),
-                                    reinterpret_cast<const uint16_t *>(Bs), lane, arow0, brow0, acc);
-    };
-    constexpr int kMfmaPerChunk = FM * FP * (sizeof(T) == 4 ? C::TK / 2 : C::TK / 16);
-    constexpr int kVmemPerChunk = C::A_PER * (sizeof(T) == 4 ? 1 : 1) + C::KR;
-    // every chunk but the last: fetch the next one while the MFMAs consume this one
-    if constexpr (SCHED == 4 && sizeof(T) == 4) {
+    if constexpr (WEAVE && sizeof(T) == 4) {
+        // every chunk but the last: the next chunk's gather is woven between this chunk's MFMAs
         BGather<C> bg;
         for (int kc = 0; kc + 1 < nchunks; ++kc) {
             const int buf = kc & 1;
@@ -440,42 +423,18 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                                     reinterpret_cast<const float *>(Bs0 + ((nchunks - 1) & 1) * C::TP * C::LDK),
                                     lane, arow0, brow0, acc, D, Wt, g, 0, KVEC, as, ra, amask, bg, bkg, pvalid,
                                     lane_base, ih0, iw0, rb);
-    } else if constexpr (SCHED == 5) {
-        // two chunks in flight: registers hold chunks kc+1 and kc+2 while chunk kc is consumed
-        Pack<T, C::VEC> ra2[C::A_PER];
-        Pack<T, C::VEC> rb2[C::KR / C::VEC];
-        uint32_t amask2 = 0, bmask2 = 0;
-        if (nchunks > 1) {
-            amask2 = load_a<C>(Wt, g, C::TK, KVEC, as, ra2);
-            bmask2 = load_b<C>(D, g, C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
-        }
-        int kc = 0;
-        for (; kc + 2 < nchunks; kc += 2) {
-            // even step: regs2 hold kc+1; fetch kc+2 into regs
-            amask = load_a<C>(Wt, g, (kc + 2) * C::TK, KVEC, as, ra);
-            bmask = load_b<C>(D, g, (kc + 2) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
-            mma(0);
-            store_lds<C>(As0 + C::TM * C::LDK, Bs0 + C::TP * C::LDK, tid, ra2, amask2, rb2, bmask2, bp, bkg);
-            __syncthreads();
-            // odd step: regs hold kc+2; fetch kc+3 into regs2
-            if (kc + 3 < nchunks) {
-                amask2 = load_a<C>(Wt, g, (kc + 3) * C::TK, KVEC, as, ra2);
-                bmask2 = load_b<C>(D, g, (kc + 3) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
-            }
-            mma(1);
-            store_lds<C>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
-            __syncthreads();
-        }
-        // kc is even; chunks kc (in LDS 0) and possibly kc+1 (in regs2) remain
-        if (kc + 1 < nchunks) {
-            mma(0);
-            store_lds<C>(As0 + C::TM * C::LDK, Bs0 + C::TP * C::LDK, tid, ra2, amask2, rb2, bmask2, bp, bkg);
-            __syncthreads();
-            mma(1);
-        } else {
-            mma(0);
-        }
     } else {
+        auto mma = [&](int buf) {
+            const T *As = As0 + buf * C::TM * C::LDK;
+            const T *Bs = Bs0 + buf * C::TP * C::LDK;
+            if constexpr (sizeof(T) == 4)
+                mma_f32<C::TK, FM, FP>(reinterpret_cast<const float *>(As), reinterpret_cast<const float *>(Bs),
+                                       lane, arow0, brow0, acc);
+            else
+                mma_bf16<C::TK, FM, FP>(reinterpret_cast<const uint16_t *>(As),
+                                        reinterpret_cast<const uint16_t *>(Bs), lane, arow0, brow0, acc);
+        };
+        // every chunk but the last: fetch the next one while the MFMAs consume this one
         for (int kc = 0; kc + 1 < nchunks; ++kc) {
             const int buf = kc & 1;
             const int kb = (kc + 1) * C::TK;
@@ -484,84 +443,227 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             mma(buf);
             store_lds<C>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
                          bmask, bp, bkg);
-            interleave<SCHED, kMfmaPerChunk, kVmemPerChunk>();
             __syncthreads();
         }
         mma((nchunks - 1) & 1);
     }
 
-    // epilogue: lane owns pixel (lane & 31) of each 32-wide block
+    // epilogue: lane owns pixel (lane & 31) of each 32-wide block; register e of
+    // block (i, j) is row 8*(e/4) + 4*(lane/32) + e%4 of that block
     const int l32 = lane & 31, h = lane >> 5;
+    if constexpr (EPI == 0) {
 #pragma unroll
-    for (int j = 0; j < FP; ++j) {
-        const long long pgo = p0 + brow0 + j * 32 + l32;
-        if (pgo >= g.P_total) continue;
-        const long long n = pgo / g.EF;
-        const long long ob = n * g.M * (long long)g.EF + (pgo - n * g.EF);
+        for (int j = 0; j < FP; ++j) {
+            const long long pgo = p0 + brow0 + j * 32 + l32;
+            if (pgo >= g.P_total) continue;
+            const long long n = pgo / g.EF;
+            const long long ob = n * g.M * (long long)g.EF + (pgo - n * g.EF);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int m = m0 + arow0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+                    if (m < g.M) Elem<T>::store(O, ob + (long long)m * g.EF, acc[i][j][e]);
+                }
+        }
+    } else {
+        using Bt = Bits<T>;
+        if (blockIdx.x == 0 && tid == 0) reset_report(ep.rep, ep.cap);
+        // faults inside this tile (a uniform test; usually none)
+        bool planted = false;
+        if constexpr (EPI == 2) {
+            for (int f = 0; f < ep.fl.n; ++f) {
+                const ftcnn_fault &q = ep.fl.f[f];
+                const long long pf = (long long)q.n * g.EF + (long long)q.x * g.F + q.y;
+                planted |= q.m >= m0 && q.m < m0 + C::TM && pf >= p0 && pf < p0 + C::TP;
+            }
+        }
+        if constexpr (WM > 1) __syncthreads();  // the LDS tiles are free: reuse them for the cross-wave fold
+        double *red = reinterpret_cast<double *>(smem);   // [WM][3][TP]
+        const double wb = (double)g.wbase;
+        // per-column state; rows are visited one register at a time (row-dependent
+        // values are then live only briefly, which keeps the kernel's register
+        // budget, and so the main loop's occupancy, close to the plain store's)
+        const int mrow = m0 + arow0 + 4 * h;
+        T *obase[FP];
+        long long pcol[FP];
+        bool cval[FP];
+        double s1[FP], s6[FP], sq[FP];
+#pragma unroll
+        for (int j = 0; j < FP; ++j) {
+            const long long pgo = p0 + brow0 + j * 32 + l32;
+            cval[j] = pgo < g.P_total;
+            const long long n = cval[j] ? pgo / g.EF : 0;
+            pcol[j] = pgo;
+            obase[j] = O + (n * g.M + mrow) * (long long)g.EF + (pgo - n * g.EF);
+            s1[j] = s6[j] = sq[j] = 0.0;
+        }
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int m = m0 + arow0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-                if (m < g.M) Elem<T>::store(O, ob + (long long)m * g.EF, acc[i][j][e]);
+                const int mo = i * 32 + 8 * (e >> 2) + (e & 3);   // row offset from mrow
+                const int m = mrow + mo;
+                const bool mok = m < g.M;
+                const double wm = (double)m + wb;
+#pragma unroll
+                for (int j = 0; j < FP; ++j) {
+                    typename Bt::B b = Bt::make(acc[i][j][e]);
+                    if constexpr (EPI == 2) {
+                        if (planted) {
+                            for (int f = 0; f < ep.fl.n; ++f) {
+                                const ftcnn_fault &q = ep.fl.f[f];
+                                const long long pf = (long long)q.n * g.EF + (long long)q.x * g.F + q.y;
+                                if (q.m == m && pf == pcol[j]) b = fault_apply(b, q);
+                            }
+                        }
+                    }
+                    if (cval[j] && mok) {
+                        const double v = (double)Bt::value(b);
+                        s1[j] += v;
+                        s6[j] = fma(wm, v, s6[j]);
+                        sq[j] = fma(v, v, sq[j]);
+                        obase[j][mo * g.EF] = b;
+                    }
+                }
             }
+#pragma unroll
+        for (int j = 0; j < FP; ++j) {
+            // rows 4..7 of every 8 sit in the other half-wave: both halves end with the same sums
+            const double a1 = s1[j] + __shfl_xor(s1[j], 32, 64);
+            const double a6 = s6[j] + __shfl_xor(s6[j], 32, 64);
+            const double aq = sq[j] + __shfl_xor(sq[j], 32, 64);
+            const int cl = brow0 + j * 32 + l32;
+            if (WM == 1) {
+                if (h == 0 && cval[j]) {
+                    const long long pgo = pcol[j];
+                    const long long n = pgo / g.EF;
+                    double *dst = ep.part + ((size_t)mt * g.N + n) * 4 * g.EF + (pgo - n * g.EF);
+                    dst[0] = a1;
+                    dst[g.EF] = a6;
+                    dst[2 * (size_t)g.EF] = ((double)n + wb) * a1;
+                    dst[3 * (size_t)g.EF] = aq;
+                }
+            } else if (h == 0) {
+                red[(wm * 3 + 0) * C::TP + cl] = a1;
+                red[(wm * 3 + 1) * C::TP + cl] = a6;
+                red[(wm * 3 + 2) * C::TP + cl] = aq;
+            }
+        }
+        if constexpr (WM > 1) {
+            __syncthreads();
+            for (int cl = tid; cl < C::TP; cl += C::NT) {
+                const long long pgo = p0 + cl;
+                if (pgo >= g.P_total) continue;
+                double s1 = 0.0, s6 = 0.0, sq = 0.0;
+#pragma unroll
+                for (int w = 0; w < WM; ++w) {
+                    s1 += red[(w * 3 + 0) * C::TP + cl];
+                    s6 += red[(w * 3 + 1) * C::TP + cl];
+                    sq += red[(w * 3 + 2) * C::TP + cl];
+                }
+                const long long n = pgo / g.EF;
+                double *dst = ep.part + ((size_t)mt * g.N + n) * 4 * g.EF + (pgo - n * g.EF);
+                dst[0] = s1;
+                dst[g.EF] = s6;
+                dst[2 * (size_t)g.EF] = ((double)n + wb) * s1;
+                dst[3 * (size_t)g.EF] = sq;
+            }
+        }
     }
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP, int SCHED, bool KVEC>
-hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major) {
+template <typename Tr, int WM, int WP, int FM, int FP, bool WEAVE, bool KVEC, int EPI>
+hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
+                      const Epi<EPI> &ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
     using T = typename C::T;
+    static_assert(EPI == 0 || (size_t)WM * 3 * C::TP * sizeof(double) <= C::LDS_BYTES, "epilogue fold fits LDS");
     const int tiles_m = (g.M + C::TM - 1) / C::TM;
     const long long tiles_p = (g.P_total + C::TP - 1) / C::TP;
     const long long total = tiles_p * tiles_m;
     if (total > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    auto kern = conv_kernel<Tr, WM, WP, FM, FP, SCHED, KVEC>;
+    auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI>;
     if constexpr (C::LDS_BYTES > 65536) {
         static const hipError_t attr = hipFuncSetAttribute(
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
         if (attr != hipSuccess) return attr;
     }
     kern<<<(unsigned)total, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D), static_cast<const T *>(W),
-                                                       static_cast<T *>(O), g, tiles_m, (int)total, m_major);
+                                                       static_cast<T *>(O), g, tiles_m, (int)total, m_major, ep);
     return hipGetLastError();
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP, int SCHED = 0>
-hipError_t run_conv(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major = 0) {
-    const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
-    if (kvec) return launch_one<Tr, WM, WP, FM, FP, SCHED, true>(g, D, W, O, st, m_major);
-    return launch_one<Tr, WM, WP, FM, FP, SCHED, false>(g, D, W, O, st, m_major);
-}
-
-}  // namespace
+// One tile configuration, dispatched on the weight alignment and the epilogue.
+template <typename Tr, int WM, int WP, int FM, int FP, bool WEAVE> struct Tile {
+    static constexpr int TM = WM * FM * 32;
+    template <int EPI>
+    static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep) {
+        const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+        if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI>(g, D, W, O, st, 0, ep);
+        return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI>(g, D, W, O, st, 0, ep);
+    }
+};
 
 // Tile choice per layer (fp32 rules from a sweep over the workload shapes on
 // MI355X): the filter tile follows M so small-M layers waste no MFMA rows; for
 // larger M the biggest tile that still leaves about two workgroups per CU wins,
 // except that layers with large W (M >= 512, K >= 4096) prefer 256-row tiles,
 // which halve the im2col traffic per flop.
-namespace {
 long long n_tiles(const Geom &g, int tm, int tp) {
     return ((g.P_total + tp - 1) / tp) * (long long)((g.M + tm - 1) / tm);
 }
+
+using F32_M32 = Tile<F32T<16>, 1, 4, 1, 2, true>;
+using F32_M64 = Tile<F32T<16>, 2, 2, 1, 2, true>;
+using F32_M96 = Tile<F32T<16>, 1, 4, 3, 2, true>;
+using F32_256x128 = Tile<F32T<16>, 4, 2, 2, 2, true>;
+using F32_128x128 = Tile<F32T<16>, 2, 2, 2, 2, true>;
+using F32_128x64 = Tile<F32T<32>, 2, 2, 2, 1, true>;
+using F32_64x64 = Tile<F32T<32>, 2, 2, 1, 1, true>;
+using BF16_M32 = Tile<BF16T<32>, 1, 4, 1, 2, false>;
+using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, false>;
+using BF16_128x128 = Tile<BF16T<32>, 2, 2, 2, 2, false>;
+
+// Calls f.template operator()<TileType>() for the tile this layer uses.
+template <typename Fn>
+auto with_tile(const Geom &g, Fn &&f) {
+    if (g.dtype == FTCNN_F32) {
+        if (g.M <= 32) return f(F32_M32{});
+        if (g.M <= 64) return f(F32_M64{});
+        if (g.M <= 96) return f(F32_M96{});
+        if (g.M >= 512 && g.K >= 4096 && n_tiles(g, 256, 128) >= 256) return f(F32_256x128{});
+        if (n_tiles(g, 128, 128) >= 600) return f(F32_128x128{});
+        if (n_tiles(g, 128, 64) >= 380) return f(F32_128x64{});
+        return f(F32_64x64{});
+    }
+    if (g.M <= 32) return f(BF16_M32{});
+    if (g.M <= 64) return f(BF16_M64{});
+    return f(BF16_128x128{});
+}
+
 }  // namespace
 
+int conv_tile_m(const Geom &g) {
+    return with_tile(g, [](auto t) { return decltype(t)::TM; });
+}
+
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st) {
-    const Geom &g = pl.g;
-    if (g.dtype == FTCNN_F32) {
-        if (g.M <= 32) return run_conv<F32T<16>, 1, 4, 1, 2, 4>(g, D, W, O, st);
-        if (g.M <= 64) return run_conv<F32T<16>, 2, 2, 1, 2, 4>(g, D, W, O, st);
-        if (g.M <= 96) return run_conv<F32T<16>, 1, 4, 3, 2, 4>(g, D, W, O, st);
-        if (g.M >= 512 && g.K >= 4096 && n_tiles(g, 256, 128) >= 256)
-            return run_conv<F32T<16>, 4, 2, 2, 2, 4>(g, D, W, O, st);
-        if (n_tiles(g, 128, 128) >= 600) return run_conv<F32T<16>, 2, 2, 2, 2, 4>(g, D, W, O, st);
-        if (n_tiles(g, 128, 64) >= 380) return run_conv<F32T<32>, 2, 2, 2, 1, 4>(g, D, W, O, st);
-        return run_conv<F32T<32>, 2, 2, 1, 1, 4>(g, D, W, O, st);
+    const Epi<0> ep{};
+    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
+}
+
+hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, ftcnn_report *rep, int cap,
+                            const ftcnn_fault *faults, int nf, void *ws, hipStream_t st) {
+    double *part = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_sums);
+    if (nf == 0) {
+        Epi<1> ep{part, rep, cap, {}};
+        return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
     }
-    if (g.M <= 32) return run_conv<BF16T<32>, 1, 4, 1, 2>(g, D, W, O, st);
-    if (g.M <= 64) return run_conv<BF16T<32>, 1, 4, 2, 2>(g, D, W, O, st);
-    return run_conv<BF16T<32>, 2, 2, 2, 2>(g, D, W, O, st);
+    Epi<2> ep{part, rep, cap, {}};
+    for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
+    ep.fl.n = nf;
+    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
 }  // namespace ftcnn

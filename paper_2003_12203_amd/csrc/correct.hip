@@ -663,13 +663,13 @@ Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftc
 
 template <typename T>
 hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums &ck,
-                     const ftcnn_policy &pol, ftcnn_report *rep, void *ws, hipStream_t st) {
+                     const ftcnn_policy &pol, ftcnn_report *rep, void *ws, size_t off_part, int sp,
+                     hipStream_t st) {
     const Ctx<T> c = make_ctx<T>(pl, D, W, O, ck, pol, rep);
     char *w = static_cast<char *>(ws);
-    const double *part = reinterpret_cast<const double *>(w + pl.off_ver);
+    const double *part = reinterpret_cast<const double *>(w + off_part);
     int *flags = reinterpret_cast<int *>(w + pl.off_flags);
     double *scratch = reinterpret_cast<double *>(w + pl.off_corr);
-    const int sp = pl.ver_splits;
     const int tpp = final_tpp(sp);
     const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
 #define VC(TPP)                                                                                          \
@@ -723,8 +723,16 @@ hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, v
                                  int cap, void *ws, hipStream_t st) {
     hipError_t e = launch_verify_partial(pl, O, rep, cap, ws, st);
     if (e != hipSuccess) return e;
-    if (pl.g.dtype == FTCNN_F32) return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, st);
-    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, st);
+    if (pl.g.dtype == FTCNN_F32) return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, st);
+}
+
+hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O,
+                                      const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
+                                      void *ws, hipStream_t st) {
+    if (pl.g.dtype == FTCNN_F32)
+        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, st);
 }
 
 }  // namespace ftcnn

@@ -31,7 +31,8 @@ struct Plan {
     int ver_cols_per_block;           // columns handled by one verify block
     int corr_blocks;                  // workgroups of the correction kernel
     int corr_slots;                   // per-workgroup scratch slices (correction or fused verification)
-    size_t off_flags, off_enc, off_ver, off_corr, bytes;
+    int sum_splits;                   // partial-sum slices written by the convolution epilogue
+    size_t off_flags, off_enc, off_ver, off_sums, off_corr, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
 
@@ -63,6 +64,36 @@ template <> struct Elem<uint16_t> {
     __device__ static void store(uint16_t *p, long long i, float v) { p[i] = f32_to_bf16_bits(v); }
 };
 
+// ---- faults planted for testing (the paper's source-level injection, Sec. 6.1)
+
+// A fault list passed by value in kernel arguments.
+struct FaultList {
+    ftcnn_fault f[kMaxFaults];
+    int n;
+};
+
+// One fault applied to a stored output pattern: kind 0 flips a bit of the
+// pattern, kind 1 adds a value, kind 2 stores a value (rounded to the dtype).
+__device__ inline float fault_apply(float v, const ftcnn_fault &f) {
+    if (f.kind == 0) return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, v) ^ (1u << f.bit));
+    return (float)(f.kind == 1 ? (double)v + f.value : f.value);
+}
+__device__ inline uint16_t fault_apply(uint16_t b, const ftcnn_fault &f) {
+    if (f.kind == 0) return (uint16_t)(b ^ (1u << f.bit));
+    return f32_to_bf16_bits((float)(f.kind == 1 ? (double)bf16_bits_to_f32(b) + f.value : f.value));
+}
+
+// A fresh report: nothing detected, cap_fixes recorded.
+__device__ inline void reset_report(ftcnn_report *rep, int cap) {
+    rep->detected = 0;
+    rep->n_flagged = 0;
+    rep->status = FTCNN_STATUS_CLEAN;
+    for (int i = 0; i < 7; ++i) rep->resolved_by[i] = 0;
+    rep->n_fixes = 0;
+    rep->cap_fixes = cap;
+    rep->reserved[0] = rep->reserved[1] = 0;
+}
+
 // ---- tolerance (the shared reading of "not equal") ------------------------
 
 __host__ __device__ inline double tol_scale(const Geom &g, double kappa) {
@@ -79,6 +110,15 @@ __device__ inline bool is_bad(double d, double q, double scale) {
 hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, double *c2,
                          void *ws, hipStream_t st);
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st);
+// The convolution with the CoC-D summations in its epilogue: every tile also
+// writes its (So5, So6, So7, sum of squares) partials for the pixels it owns to
+// the workspace (pl.sum_splits slices, layout of the verification partials) and
+// the report is reset.  faults (at most kMaxFaults, host array) are planted in
+// the stored values before they are summed.
+hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, ftcnn_report *rep, int cap,
+                            const ftcnn_fault *faults, int nf, void *ws, hipStream_t st);
+// Rows of C per workgroup tile of the convolution chosen for this layer.
+int conv_tile_m(const Geom &g);
 hipError_t launch_checksum_conv(const Plan &pl, uint32_t which, const void *D, const void *W,
                                 const ftcnn_checksums &ck, hipStream_t st);
 hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &ck,
@@ -92,6 +132,10 @@ hipError_t launch_verify_partial(const Plan &pl, const void *O, ftcnn_report *re
 hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, void *O,
                                  const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
                                  int cap, void *ws, hipStream_t st);
+// Final detection stage and correction over the partials the convolution epilogue wrote.
+hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O,
+                                      const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
+                                      void *ws, hipStream_t st);
 
 // Threads that share one position in the final verification stage (a power of
 // two; the float64 split partials of that position are spread over them).

@@ -6,29 +6,13 @@
 namespace ftcnn {
 namespace {
 
-struct FaultList {
-    ftcnn_fault f[kMaxFaults];
-    int n;
-};
-
 template <typename T>
 __global__ void inject_kernel(T *O, Geom g, FaultList fl) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     for (int i = 0; i < fl.n; ++i) {
         const ftcnn_fault &f = fl.f[i];
         const long long idx = (((long long)f.n * g.M + f.m) * g.E + f.x) * g.F + f.y;
-        if (f.kind == 0) {
-            if constexpr (sizeof(T) == 4) {
-                const uint32_t b = __builtin_bit_cast(uint32_t, O[idx]) ^ (1u << f.bit);
-                O[idx] = __builtin_bit_cast(float, b);
-            } else {
-                O[idx] = (T)(O[idx] ^ (uint16_t)(1u << f.bit));
-            }
-        } else {
-            const double old = (double)Elem<T>::load(O, idx);
-            const double v = f.kind == 1 ? old + f.value : f.value;
-            Elem<T>::store(O, idx, (float)v);
-        }
+        O[idx] = fault_apply(O[idx], f);
     }
 }
 

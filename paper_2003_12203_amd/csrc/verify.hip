@@ -39,16 +39,6 @@ template <> struct VLoad<uint16_t, 8> {
     }
 };
 
-__device__ inline void reset_report(ftcnn_report *rep, int cap) {
-    rep->detected = 0;
-    rep->n_flagged = 0;
-    rep->status = FTCNN_STATUS_CLEAN;
-    for (int i = 0; i < 7; ++i) rep->resolved_by[i] = 0;
-    rep->n_fixes = 0;
-    rep->cap_fixes = cap;
-    rep->reserved[0] = rep->reserved[1] = 0;
-}
-
 template <typename T, int VEC>
 __global__ __launch_bounds__(kThreads) void verify_partial(const T *__restrict__ O, Geom g, int ctt,
                                                            double *__restrict__ part,

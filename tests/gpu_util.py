@@ -2,10 +2,12 @@
 from __future__ import annotations
 
 import numpy as np
+import pytest
 import torch
 
 import paper_2003_12203_amd as ft
 import workloads as wl
+from oracle import core
 from oracle import workflow as wf
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
@@ -62,3 +64,30 @@ def oracle_policy_from(pol: ft._lib.Policy, wbase: int = 0) -> wf.Policy:
     return wf.Policy(rc_on=bool(pol.rc_on), clc_on=bool(pol.clc_on),
                      repair="recompute" if pol.repair == ft.REPAIR_RECOMPUTE else "checksum",
                      kappa=pol.kappa, eta=pol.eta, wbase=wbase)
+
+
+def workload_shapes():
+    """Distinct layer shapes of all workloads, shrunk (batch, then spatial crop) to about a GFLOP."""
+    seen, out = set(), []
+    cfgs = wl.configs() + [wl.vgg19_bf16()]
+    for cfg in cfgs:
+        for li, L in enumerate(cfg.layers):
+            key = (L.ch, L.h, L.m, L.r, L.stride, L.pad, L.dtype)
+            if key in seen:
+                continue
+            seen.add(key)
+            spec = L
+            for n in (3, 2, 1):
+                spec = spec.with_(n=min(n, L.n))
+                E = core.out_extent(spec.h, spec.r, spec.stride, spec.pad)
+                if 2 * spec.n * spec.m * E * E * spec.ch * spec.r * spec.s <= 1.5e9:
+                    break
+            h = spec.h
+            while True:
+                E = core.out_extent(h, spec.r, spec.stride, spec.pad)
+                if 2 * spec.n * spec.m * E * E * spec.ch * spec.r * spec.s <= 1.5e9 or h <= 2 * spec.r:
+                    break
+                h = int(h * 0.8)
+            spec = spec.with_(h=h, w=h)
+            out.append(pytest.param(cfg, li, spec, id=f"{cfg.name}-{L.name}-n{spec.n}-h{spec.h}"))
+    return out

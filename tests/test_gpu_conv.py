@@ -4,41 +4,14 @@ import pytest
 import torch
 
 import workloads as wl
-from gpu_util import TOL, assert_close_scaled, dev, host, layer_for
+from gpu_util import TOL, assert_close_scaled, dev, host, layer_for, workload_shapes
 from oracle import core
 from oracle import workflow as wf
 
 pytestmark = pytest.mark.gpu
 
 
-def _shapes():
-    """Distinct layer shapes of all workloads, shrunk (batch, then spatial crop) to about a GFLOP."""
-    seen, out = set(), []
-    cfgs = wl.configs() + [wl.vgg19_bf16()]
-    for cfg in cfgs:
-        for li, L in enumerate(cfg.layers):
-            key = (L.ch, L.h, L.m, L.r, L.stride, L.pad, L.dtype)
-            if key in seen:
-                continue
-            seen.add(key)
-            spec = L
-            for n in (3, 2, 1):
-                spec = spec.with_(n=min(n, L.n))
-                E = core.out_extent(spec.h, spec.r, spec.stride, spec.pad)
-                if 2 * spec.n * spec.m * E * E * spec.ch * spec.r * spec.s <= 1.5e9:
-                    break
-            h = spec.h
-            while True:
-                E = core.out_extent(h, spec.r, spec.stride, spec.pad)
-                if 2 * spec.n * spec.m * E * E * spec.ch * spec.r * spec.s <= 1.5e9 or h <= 2 * spec.r:
-                    break
-                h = int(h * 0.8)
-            spec = spec.with_(h=h, w=h)
-            out.append(pytest.param(cfg, li, spec, id=f"{cfg.name}-{L.name}-n{spec.n}-h{spec.h}"))
-    return out
-
-
-@pytest.mark.parametrize("cfg,li,spec", _shapes())
+@pytest.mark.parametrize("cfg,li,spec", workload_shapes())
 def test_conv_matches_oracle(cfg, li, spec):
     D = wl.gen_d(cfg, li, spec)
     W = wl.gen_w(cfg, li, spec)

@@ -1,0 +1,185 @@
+"""The convolution with the CoC-D summations in its epilogue (ftcnn_conv_fwd_sums) against the
+separate kernels and the oracle.
+
+* O is bitwise the output of ftcnn_conv_fwd (same main loop, same rounding);
+* So5, So6, So7 and Q5 from the epilogue partials agree with the oracle's summations of the
+  GPU's own output (Sec. 3.6) to float64 rounding, and exactly on integer data;
+* faults planted in the epilogue give bitwise the output that ftcnn_inject gives afterwards;
+* ftcnn_protected_conv (the whole path in one call) matches the step-by-step path.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2003_12203_amd as ft
+import workloads as wl
+from gpu_util import assert_close_scaled, dev, gpu_flags, host, layer_for, to_ft_faults, workload_shapes
+from oracle import workflow as wf
+
+pytestmark = pytest.mark.gpu
+
+
+def _sums(lay):
+    torch.cuda.synchronize()
+    return {k: lay.buf[k].cpu().numpy().copy() for k in ("so5", "so6", "so7", "q5")}
+
+
+@pytest.mark.parametrize("cfg,li,spec", workload_shapes())
+@pytest.mark.parametrize("wbase", [0, 1])
+def test_epilogue_sums_match_oracle(cfg, li, spec, wbase):
+    D, W = wl.gen_d(cfg, li, spec), wl.gen_w(cfg, li, spec)
+    lay = layer_for(spec, wbase=wbase)
+    Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
+    lay.encode_weights(Wd)
+    lay.encode_input(Dd)
+    O_ref = lay.empty_output()
+    lay.conv(Dd, Wd, O_ref)
+    O = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O)
+    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+    lay.verify_correct_sums(Dd, Wd, O)
+    torch.cuda.synchronize()
+    assert torch.equal(O.view(torch.int16 if spec.dtype == "bf16" else torch.int32),
+                       O_ref.view(torch.int16 if spec.dtype == "bf16" else torch.int32)), "O differs from conv_fwd"
+    got = _sums(lay)
+    co5 = lay.buf["co5"].cpu().numpy().reshape(lay.E, lay.F)
+    so5, so6, so7, q5, flags = wf.verify(host(O), co5, spec.ch * spec.r * spec.s, spec.dtype,
+                                         wf.Policy(wbase=wbase))
+    for name, ref in [("so5", so5), ("so6", so6), ("so7", so7), ("q5", q5)]:
+        assert_close_scaled(got[name].reshape(ref.shape), ref, 1e-11, name)
+    assert not flags.any(), "clean layer flagged by the oracle"
+    assert not gpu_flags(lay).any(), "clean layer flagged by the GPU"
+    rep = lay.read_report()
+    assert not rep.detected and rep.status == ft.STATUS_CLEAN and rep.n_flagged == 0
+
+
+@pytest.mark.parametrize("shape", [
+    # n, ch, h, m, r, stride, pad: ragged pixel tails, partial filter tiles, several tiles per image
+    (5, 6, 12, 9, 3, 1, 1),
+    (3, 16, 10, 5, 3, 1, 1),
+    (2, 7, 9, 33, 3, 2, 1),
+    (4, 64, 7, 130, 1, 1, 0),
+    (1, 3, 35, 96, 11, 4, 0),
+    (2, 8, 13, 200, 5, 3, 2),
+    (2, 5, 3, 7, 3, 1, 0),       # E = 1
+])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_epilogue_sums_integer_exact(shape, dtype):
+    """Integer data: the epilogue's summations equal the checksum convolutions exactly."""
+    n, ch, h, m, r, u, p = shape
+    spec = wl.LayerSpec("int", n, ch, h, h, m, r, r, u, p, dtype)
+    D, W = wl.gen_int_d(spec, 7 + sum(shape)), wl.gen_int_w(spec, 7 + sum(shape))
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, dtype), dev(W, dtype)
+    lay.encode_weights(Wd)
+    lay.encode_input(Dd)
+    O = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O)
+    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+    lay.verify_correct_sums(Dd, Wd, O)
+    torch.cuda.synchronize()
+    b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
+    if dtype == "f32" or np.abs(host(O)).max() <= 256:
+        np.testing.assert_array_equal(b["co5"], b["so5"])
+        np.testing.assert_array_equal(b["co6"], b["so6"])
+        np.testing.assert_array_equal(b["co7"], b["so7"])
+    assert not lay.read_report().detected
+
+
+def test_epilogue_sums_deterministic():
+    cfg = wl.config(1)
+    spec = cfg.layers[1].with_(n=6)
+    lay = layer_for(spec)
+    Dd, Wd = dev(wl.gen_d(cfg, 1, spec), "f32"), dev(wl.gen_w(cfg, 1, spec), "f32")
+    lay.encode_weights(Wd)
+    lay.encode_input(Dd)
+    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+    O = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O)
+    lay.verify_correct_sums(Dd, Wd, O)
+    first = _sums(lay)
+    lay.conv_sums(Dd, Wd, O)
+    lay.verify_correct_sums(Dd, Wd, O)
+    second = _sums(lay)
+    for k in first:
+        np.testing.assert_array_equal(first[k], second[k])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_planted_faults_equal_injected(dtype):
+    """Faults planted in the epilogue (every kind, repeated hits on one element, NaN-producing
+    flips) leave exactly the output that ftcnn_inject leaves on the plain convolution."""
+    spec = wl.LayerSpec("f", 3, 8, 11, 11, 70, 3, 3, 1, 1, dtype)
+    cfg = wl.Config(92, "f", (spec,), "uniform", "he")
+    D, W = wl.gen_d(cfg, 0, spec), wl.gen_w(cfg, 0, spec)
+    top = 30 if dtype == "f32" else 14
+    faults = [
+        wf.Fault(0, 0, 0, 0, "flip", top),
+        wf.Fault(2, 69, 10, 10, "add", value=-3.5),
+        wf.Fault(1, 33, 5, 7, "set", value=123.25),
+        wf.Fault(1, 33, 5, 7, "add", value=0.5),          # second hit on one element
+        wf.Fault(2, 64, 3, 9, "flip", top - 1),
+        wf.Fault(0, 5, 4, 4, "set", value=float("inf")),
+    ]
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, dtype), dev(W, dtype)
+    lay.encode_weights(Wd)
+    lay.encode_input(Dd)
+    O1 = lay.empty_output()
+    lay.conv(Dd, Wd, O1)
+    lay.inject(O1, to_ft_faults(faults))
+    O2 = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O2, to_ft_faults(faults))
+    torch.cuda.synchronize()
+    iv = torch.int16 if dtype == "bf16" else torch.int32
+    assert torch.equal(O1.view(iv), O2.view(iv))
+    O_faulty = host(O2)
+    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+    lay.verify_correct_sums(Dd, Wd, O2)
+    rep = lay.read_report()
+    # the decisions on the planted faults are the oracle's on the same faulted output (a flip that
+    # shrinks a bf16 value may stay inside the bf16 tolerance and go undetected on both sides)
+    ores = wf.protect(D, W, spec.stride, spec.pad, dtype, O_in=O_faulty).report
+    assert rep.detected and ores.detected
+    assert rep.n_flagged == ores.n_flagged and rep.fixes == ores.fixes
+
+
+def test_fault_list_is_validated():
+    spec = wl.LayerSpec("v", 2, 3, 8, 8, 4, 3, 3, 1, 1, "f32")
+    lay = layer_for(spec)
+    D = torch.zeros(spec.n, spec.ch, spec.h, spec.w, device="cuda")
+    W = torch.zeros(spec.m, spec.ch, spec.r, spec.s, device="cuda")
+    O = lay.empty_output()
+    with pytest.raises(ft.FtcnnError, match="out of range"):
+        lay.conv_sums(D, W, O, [{"n": 2, "m": 0, "x": 0, "y": 0, "kind": "add", "value": 1.0}])
+    with pytest.raises(ft.FtcnnError, match="bit"):
+        lay.conv_sums(D, W, O, [{"n": 0, "m": 0, "x": 0, "y": 0, "kind": "flip", "bit": 32}])
+    with pytest.raises(ft.FtcnnError, match="at most"):
+        lay.conv_sums(D, W, O, [{"n": 0, "m": 0, "x": 0, "y": 0, "kind": "add", "value": 1.0}] * 65)
+
+
+@pytest.mark.parametrize("li", [0, 1, 2])
+def test_protected_conv_single_call(li):
+    """ftcnn_protected_conv equals the step-by-step path (AlexNet layers, reduced batch)."""
+    cfg = wl.config(1)
+    spec = cfg.layers[li].with_(n=3)
+    D, W = wl.gen_d(cfg, li, spec), wl.gen_w(cfg, li, spec)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, "f32"), dev(W, "f32")
+    lay.encode_weights(Wd)
+    O = lay.empty_output()
+    lay.protected(Dd, Wd, O)
+    one = _sums(lay)
+    rep = lay.read_report()
+    assert not rep.detected and rep.status == ft.STATUS_CLEAN
+    O2 = lay.empty_output()
+    lay.encode_input(Dd)
+    lay.conv(Dd, Wd, O2)
+    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+    lay.verify(O2)
+    torch.cuda.synchronize()
+    assert torch.equal(O, O2)
+    two = _sums(lay)
+    Q = two["q5"]
+    for k in ("so5", "so6", "so7"):
+        np.testing.assert_allclose(one[k], two[k], rtol=0, atol=1e-12 * float(Q.max()) * max(spec.n, spec.m))

@@ -1,5 +1,12 @@
 """GPU detection and correction decisions against the oracle (Sec. 4.1 scenarios and seeded faults).
 
+Every case runs through each of the library's detection paths:
+
+* ``separate``: ftcnn_verify then ftcnn_correct, faults injected into the stored O;
+* ``fused``: ftcnn_verify_correct (one detection read of O, correction in the same launch);
+* ``epilogue``: ftcnn_conv_fwd_sums (summations in the convolution's epilogue, faults planted
+  in its outputs before they are summed) then ftcnn_verify_correct_sums.
+
 Decisions are compared in decision-oracle mode: the oracle's workflow runs on
 the GPU's own faulted output (before correction), so only the float64 order of
 summation differs between the two sides.  Decisions, located indices and the
@@ -29,7 +36,10 @@ def _flat(spec, target, index):
     return (c * spec.r + r) * spec.s + s
 
 
-def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None):
+MODES = ["separate", "fused", "epilogue"]
+
+
+def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None, mode="separate"):
     """Protected layer on the GPU; returns (first report, final status, faulted O, final O, flags)."""
     lay = layer_for(spec, wbase=wbase, **pol_kw)
     Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
@@ -44,19 +54,32 @@ def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None):
         else:
             lay.buf[t][_flat(spec, t, hook["index"])] += hook["add"]
     O = lay.empty_output()
-    lay.conv(Dd, Wd, O)
-    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
-    if faults:
-        lay.inject(O, to_ft_faults(faults))
-    O_faulty = host(O)
-    lay.verify(O)
-    lay.correct(Dd, Wd, O)
+    if mode == "epilogue":
+        lay.conv_sums(Dd, Wd, O, to_ft_faults(faults))
+        O_faulty = host(O)
+        lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+        lay.verify_correct_sums(Dd, Wd, O)
+    else:
+        lay.conv(Dd, Wd, O)
+        lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
+        if faults:
+            lay.inject(O, to_ft_faults(faults))
+        O_faulty = host(O)
+        if mode == "fused":
+            lay.verify_correct(Dd, Wd, O)
+        else:
+            lay.verify(O)
+            lay.correct(Dd, Wd, O)
     rep = lay.read_report()
     flags = gpu_flags(lay)
     status = rep.status
     if status == ft.STATUS_NEEDS_RECOMPUTE:
-        lay.conv(Dd, Wd, O)
-        lay.verify(O)
+        if mode == "epilogue":
+            lay.conv_sums(Dd, Wd, O)
+            lay.verify_correct_sums(Dd, Wd, O)
+        else:
+            lay.conv(Dd, Wd, O)
+            lay.verify(O)
         status = ft.STATUS_FAILED if lay.read_report().detected else ft.STATUS_RECOMPUTED
     return rep, status, O_faulty, host(O), flags
 
@@ -77,12 +100,13 @@ def compare(spec, D, W, rep, status, O_faulty, O_final, flags, policy, hook_fn=N
     return res
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("scn", SCN, ids=[s.name for s in SCN])
-def test_scenario_matches_oracle(scn):
+def test_scenario_matches_oracle(scn, mode):
     D, W = scn.inputs()
     pol = scn.oracle_policy()
     kw = dict(rc_on=pol.rc_on, clc_on=pol.clc_on, repair=pol.repair, kappa=pol.kappa, eta=pol.eta)
-    rep, status, O_faulty, O_final, flags = run_gpu(scn.spec, D, W, scn.faults, kw, pol.wbase, scn.hook)
+    rep, status, O_faulty, O_final, flags = run_gpu(scn.spec, D, W, scn.faults, kw, pol.wbase, scn.hook, mode)
     res = compare(scn.spec, D, W, rep, status, O_faulty, O_final, flags, pol, scn.oracle_hook(),
                   exact=scn.data == "int")
     # and the outcome Sec. 4.1 predicts
@@ -111,8 +135,9 @@ def _bitflip_faults(O, draws, dtype):
     return out
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("trial", range(12))
-def test_tiny_bitflip_detected_and_corrected(trial):
+def test_tiny_bitflip_detected_and_corrected(trial, mode):
     """The single-layer workload: one seeded bit flip in O, detected and corrected as the oracle does."""
     cfg = wl.config(0)
     spec = cfg.layers[0]
@@ -121,7 +146,7 @@ def test_tiny_bitflip_detected_and_corrected(trial):
     faults = _bitflip_faults(clean, wl.fault_draws(0, 0, 1, variant=trial + 1), "f32")
     if not faults:
         pytest.skip("draw produced a non-finite or no-op flip")
-    rep, status, O_faulty, O_final, flags = run_gpu(spec, D, W, faults, {})
+    rep, status, O_faulty, O_final, flags = run_gpu(spec, D, W, faults, {}, mode=mode)
     compare(spec, D, W, rep, status, O_faulty, O_final, flags, wf.Policy())
     assert rep.detected and status == ft.STATUS_CORRECTED
     assert_close_scaled(O_final, clean, 1e-4, "recovered O")
@@ -147,8 +172,9 @@ def _pattern_faults(O, draws, count):
     return out
 
 
+@pytest.mark.parametrize("mode", ["fused", "epilogue"])
 @pytest.mark.parametrize("li", [1, 5, 13, 14])
-def test_darknet_multi_fault(li):
+def test_darknet_multi_fault(li, mode):
     """Darknet-shaped layers (reduced batch and size) with seeded multi-fault injection."""
     cfg = wl.config(4)
     L = cfg.layers[li]
@@ -157,18 +183,19 @@ def test_darknet_multi_fault(li):
     clean = wf.protect(D, W, spec.stride, spec.pad, spec.dtype).O_clean
     draws = wl.fault_draws(4, li, 4)
     faults = _pattern_faults(clean, draws, 2 + int(draws[0, 6] * 3))
-    rep, status, O_faulty, O_final, flags = run_gpu(spec, D, W, faults, {})
+    rep, status, O_faulty, O_final, flags = run_gpu(spec, D, W, faults, {}, mode=mode)
     compare(spec, D, W, rep, status, O_faulty, O_final, flags, wf.Policy())
     assert rep.detected
     assert status in (ft.STATUS_CORRECTED, ft.STATUS_RECOMPUTED)
     assert_close_scaled(O_final, clean, 1e-3, "recovered O")
 
 
-def test_correct_is_noop_when_clean():
+@pytest.mark.parametrize("mode", MODES)
+def test_correct_is_noop_when_clean(mode):
     spec = wl.config(1).layers[3].with_(n=2)
     cfg = wl.config(1)
     D, W = wl.gen_d(cfg, 3, spec), wl.gen_w(cfg, 3, spec)
-    rep, status, O_faulty, O_final, flags = run_gpu(spec, D, W, [], {})
+    rep, status, O_faulty, O_final, flags = run_gpu(spec, D, W, [], {}, mode=mode)
     assert not rep.detected and status == ft.STATUS_CLEAN and rep.fixes == []
     np.testing.assert_array_equal(O_faulty, O_final)
 
