@@ -93,21 +93,53 @@ template <typename T> __device__ inline long long oidx(const Ctx<T> &c, int n, i
     return ((long long)n * c.g.M + m) * c.g.EF + p;
 }
 
+// Visits every block (n, m) of position p: thread t takes the elements
+// e = n*M + m = t, t + kThreads, ..., with (n, m) advanced incrementally and
+// eight loads in flight, and calls f(n, m, value) in that order.
+template <typename T, typename F> __device__ inline void for_blocks(const Ctx<T> &c, int p, F &&f) {
+    const Geom &g = c.g;
+    const int nm = g.N * g.M;
+    const int dn = kThreads / g.M, dm = kThreads - dn * g.M;
+    int e = threadIdx.x;
+    int n = e / g.M, m = e - n * g.M;
+    const T *col = c.O + p;
+    const long long step = (long long)kThreads * g.EF;
+    long long off = (long long)e * g.EF;
+    constexpr int U = 8;
+    for (; e + (U - 1) * kThreads < nm; e += U * kThreads) {
+        double v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = ldo(col, off + u * step);
+        off += U * step;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            f(n, m, v[u]);
+            n += dn;
+            m += dm;
+            if (m >= g.M) { m -= g.M; ++n; }
+        }
+    }
+    for (; e < nm; e += kThreads, off += step) {
+        f(n, m, ldo(col, off));
+        n += dn;
+        m += dm;
+        if (m >= g.M) { m -= g.M; ++n; }
+    }
+}
+
 // So5, So6, So7 and their Q (root sums of squares of the weighted terms) at p.
 template <typename T> __device__ void sums6(const Ctx<T> &c, int p, Sh &sh, double (&s)[6]) {
     double v[6] = {0, 0, 0, 0, 0, 0};
-    const long long nm = (long long)c.g.N * c.g.M;
-    for (long long e = threadIdx.x; e < nm; e += kThreads) {
-        const int n = (int)(e / c.g.M), m = (int)(e - (long long)n * c.g.M);
-        const double o = ldo(c.O, e * c.g.EF + p);
-        const double t6 = (double)(m + c.wb) * o, t7 = (double)(n + c.wb) * o;
+    const double wb = (double)c.wb;
+    for_blocks(c, p, [&](int n, int m, double o) {
+        const double t6 = ((double)m + wb) * o, t7 = ((double)n + wb) * o;
         v[0] += o;
         v[1] += t6;
         v[2] += t7;
         v[3] = fma(o, o, v[3]);
         v[4] = fma(t6, t6, v[4]);
         v[5] = fma(t7, t7, v[5]);
-    }
+    });
     bsum<6>(v, sh);
     s[0] = v[0]; s[1] = v[1]; s[2] = v[2];
     s[3] = sqrt(v[3]); s[4] = sqrt(v[4]); s[5] = sqrt(v[5]);
@@ -192,6 +224,7 @@ template <typename T> __device__ void row_arrays(const Ctx<T> &c, int p, int x, 
     }
     for (int m = threadIdx.x; m < g.M; m += kThreads) {
         double s1 = 0.0, s3 = 0.0, q = 0.0;
+#pragma unroll 8
         for (int n = 0; n < g.N; ++n) {
             const double o = ldo(c.O, oidx(c, n, m, p));
             s1 += o;
@@ -236,6 +269,7 @@ template <typename T> __device__ void col_arrays(const Ctx<T> &c, int p, int x, 
     }
     for (int n = threadIdx.x; n < g.N; n += kThreads) {
         double s2 = 0.0, s4 = 0.0, q = 0.0;
+#pragma unroll 8
         for (int m = 0; m < g.M; ++m) {
             const double o = ldo(c.O, oidx(c, n, m, p));
             s2 += o;
@@ -360,9 +394,9 @@ __device__ bool scheme_coc(const Ctx<T> &c, Sh &sh, int p, int x, int y, const d
         v = a[0];
     } else {
         double a[1] = {0.0};
-        const long long nm = (long long)c.g.N * c.g.M, skip = (long long)i * c.g.M + j;
-        for (long long e = threadIdx.x; e < nm; e += kThreads)
-            if (e != skip) a[0] += ldo(c.O, e * c.g.EF + p);
+        for_blocks(c, p, [&](int n, int m, double o) {
+            if (n != i || m != j) a[0] += o;
+        });
         bsum<1>(a, sh);
         v = co[0] - a[0];
     }
@@ -465,11 +499,13 @@ template <typename T> __device__ void fresh_coc(const Ctx<T> &c, int x, int y, S
         if (ih < 0 || ih >= g.H || iw < 0 || iw >= g.W) continue;
         const long long off = ((long long)ch * g.H + ih) * g.W + iw;
         double a1 = 0.0, a2 = 0.0, b1 = 0.0, b2 = 0.0;
+#pragma unroll 8
         for (int n = 0; n < g.N; ++n) {
             const double dv = ldo(c.D, (long long)n * g.CHW + off);
             a1 += dv;
             a2 = fma((double)(n + c.wb), dv, a2);
         }
+#pragma unroll 8
         for (int m = 0; m < g.M; ++m) {
             const double wv = ldo(c.W, (long long)m * g.K + k);
             b1 += wv;
