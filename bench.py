@@ -6,10 +6,12 @@ Workload: the AlexNet-shaped stack of five convolution layers, fp32, batch 64
 shape; layers are independent).  One step runs the whole protected path of
 every layer on one stream:
 
-    encode(D) -> conv_fwd_sums -> checksum_conv(Co5, Co6, Co7) -> verify_correct_sums
+    conv_fwd_sums (+ encode of Cd1, Cd2) -> verify_correct_sums (+ Co5, Co6, Co7)
 
-(the CoC-D summations in the convolution's epilogue, then one launch for the
-final detection stage and the correction chain), following the paper's
+(two launches: the input checksums are encoded by extra workgroups of the
+convolution launch and the CoC-D summations are taken in its epilogue; the
+final launch computes the checksum-of-checksums Co5..Co7, tests every position
+and runs the correction chain where one is flagged), following the paper's
 error-injection protocol (Sec. 6.1): step i corrupts one output element of
 layer (i mod 5) inside the convolution, before its output is summed, so every
 step also detects, locates and repairs one fault.  Weight checksums are encoded
@@ -106,32 +108,21 @@ def main():
     def protected_step(i, inject=True, ev=None):
         for li, r in enumerate(runs):
             L = r.lay
-            L.encode_input(r.D)
             if ev is not None and li == dom:
                 ev[0].record()
-            L.conv_sums(r.D, r.W, r.O, [r.fault] if inject and li == i % nl else ())
+            L.conv_sums(r.D, r.W, r.O, [r.fault] if inject and li == i % nl else (), encode=True)
             if ev is not None and li == dom:
                 ev[1].record()
-            L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
-            L.verify_correct_sums(r.D, r.W, r.O)
+            L.verify_correct_sums(r.D, r.W, r.O, coc=True)
 
-    def reread_step(i):
-        # the same path with detection re-reading O (ftcnn_verify_correct), error-free
+    def separate_step(i):
+        # the same path from the separate kernels (detection re-reads O), error-free
         for r in runs:
             L = r.lay
             L.encode_input(r.D)
             L.conv(r.D, r.W, r.O)
             L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
             L.verify_correct(r.D, r.W, r.O)
-
-    side = torch.cuda.Stream()
-    done = [torch.cuda.Event() for _ in runs]
-
-    def overlapped_step(i, inject=True):
-        for li, r in enumerate(runs):
-            f = [r.fault] if inject and li == i % nl else ()
-            r.lay.protected_overlapped(r.D, r.W, r.O, side, f, done[li])
-            done[li].record()
 
     def conv_step(ev=None):
         for li, r in enumerate(runs):
@@ -180,14 +171,10 @@ def main():
     # ---- reference loops: error-free protected, unprotected --------------------------
     t_clean = timed(lambda i: protected_step(i, False), args.steps)
     t_unprot = timed(lambda i: conv_step(), args.steps)
-    t_reread = timed(reread_step, args.steps)
-    t_ovl = timed(lambda i: overlapped_step(i, True), args.steps)
-    ovl_rep = runs[(args.steps - 1) % nl].lay.read_report()
-    ovl_ok = ovl_rep.detected and ovl_rep.status == ft.STATUS_CORRECTED
-    t_ovl_clean = timed(lambda i: overlapped_step(i, False), args.steps)
+    t_sep = timed(separate_step, args.steps)
 
     # ---- per-layer stage breakdown (events between the calls) ------------------------
-    stages = ["encode", "conv_sums", "checksum_conv", "verify_correct_sums"]
+    stages = ["conv_sums_encode", "verify_correct_sums_coc"]
     reps = max(3, min(args.steps, 10))
     stage_ms = np.zeros((reps, nl, len(stages)))
     for k in range(reps):
@@ -196,14 +183,10 @@ def main():
             L = r.lay
             e = evs[li]
             e[0].record()
-            L.encode_input(r.D)
+            L.conv_sums(r.D, r.W, r.O, encode=True)
             e[1].record()
-            L.conv_sums(r.D, r.W, r.O)
+            L.verify_correct_sums(r.D, r.W, r.O, coc=True)
             e[2].record()
-            L.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
-            e[3].record()
-            L.verify_correct_sums(r.D, r.W, r.O)
-            e[4].record()
         torch.cuda.synchronize()
         for li in range(nl):
             for s in range(len(stages)):
@@ -222,9 +205,7 @@ def main():
 
     per_layer = []
     for li, r in enumerate(runs):
-        spec = r.spec
         prot_t = float(stage_med[li].sum())
-        enc_bytes = 4.0 * spec.n * spec.ch * spec.h * spec.w
         per_layer.append({
             "layer": r.name, "gflop": round(r.flops / 1e9, 3),
             "conv_ms": round(float(plain_med[li]), 4),
@@ -233,7 +214,6 @@ def main():
             "protected_tflops": round(r.flops / prot_t / 1e9, 2),
             "overhead_pct": round((prot_t / float(plain_med[li]) - 1) * 100, 2),
             "stage_ms": {s: round(float(stage_med[li][k]), 4) for k, s in enumerate(stages)},
-            "encode_gbps": round(enc_bytes / float(stage_med[li][0]) / 1e6, 1),
         })
 
     # ---- roofline of the dominant kernel (its 128x128-tile kernel runs no other layer here)
@@ -242,7 +222,7 @@ def main():
     achieved = dom_flops / (dom_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_PEAK_F32, "unit": "TFLOP/s",
                 "frac": round(achieved / MFMA_PEAK_F32, 4), "traffic": measured_traffic(),
-                "kernel": f"conv_kernel fp32 128x128 tile, CoC-D sums in the epilogue ({runs[dom].name})",
+                "kernel": f"conv_kernel fp32 128x128 tile with the CoC-D sums epilogue and the encode workgroups ({runs[dom].name})",
                 "flop_per_launch": dom_flops, "avg_launch_ms": round(dom_ms, 4),
                 "all_conv_tflops": round(total_flops / (float(plain_med.sum()) * 1e-3) / 1e12, 2)}
 
@@ -271,15 +251,10 @@ def main():
         "unprotected_tflops": round(total_flops / t_unprot / 1e12, 3),
         "overhead_error_free_pct": round((t_clean / t_unprot - 1) * 100, 2),
         "overhead_erroneous_pct": round((t_prot / t_unprot - 1) * 100, 2),
-        "reread_verify": {"error_free_tflops": round(total_flops / t_reread / 1e12, 3),
-                          "overhead_error_free_pct": round((t_reread / t_unprot - 1) * 100, 2),
-                          "note": "detection re-reads O (ftcnn_verify_correct) instead of epilogue sums"},
-        "overlapped": {"tflops": round(total_flops / t_ovl / 1e12, 3),
-                       "error_free_tflops": round(total_flops / t_ovl_clean / 1e12, 3),
-                       "overhead_erroneous_pct": round((t_ovl / t_unprot - 1) * 100, 2),
-                       "overhead_error_free_pct": round((t_ovl_clean / t_unprot - 1) * 100, 2),
-                       "fault_corrected": bool(ovl_ok),
-                       "note": "encode(D) and Co5-Co7 on a second stream, concurrent with conv_fwd_sums"},
+        "separate_kernels": {"error_free_tflops": round(total_flops / t_sep / 1e12, 3),
+                             "overhead_error_free_pct": round((t_sep / t_unprot - 1) * 100, 2),
+                             "note": "encode, conv_fwd, checksum_conv(Co5-Co7), verify_correct: "
+                                     "five launches per layer, detection re-reads O"},
         "fault_corrected": bool(ok_fault),
         "clean_layers_clean": bool(clean_ok),
         "per_layer": per_layer,

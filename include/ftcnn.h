@@ -114,7 +114,7 @@ typedef struct {
     int32_t resolved_by[7];    /* positions per FTCNN_SCHEME_*                    */
     int32_t n_fixes;
     int32_t cap_fixes;
-    int32_t reserved[2];
+    int32_t reserved[2];       /* internal to the library (zeroed with the report)  */
     ftcnn_fix fixes[];
 } ftcnn_report;
 
@@ -206,32 +206,40 @@ int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void 
                          const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                          int32_t cap_fixes, void *workspace, hipStream_t stream);
 
-/* Eq. (1) as ftcnn_conv_fwd (same kernel, bitwise the same O), with the
+/* Eq. (1) as ftcnn_conv_fwd (same main loop, bitwise the same O), with the
  * CoC-D summations of Sec. 3.6 computed in the epilogue from the values as
  * stored: every workgroup tile writes, for each of its output pixels, the
  * partial So5, So6, So7 and sum of squares over its filters into the
  * workspace, so detection never re-reads O.  Also resets *rep (cap_fixes
  * recorded).  Follow it with ftcnn_verify_correct_sums on the same workspace
  * and report.
+ * ck: may be NULL.  When ck->cd1 and ck->cd2 are set, additional workgroups of
+ * the same launch encode them from D as ftcnn_encode(which = 0) does (Sec.
+ * 3.2), beside the matrix-core tiles; other members are not used.
  * faults / nf: TEST ONLY, NULL / 0 otherwise.  A HOST array of at most 64
  * faults planted in the output values before they are summed and stored, as
  * a fault of the convolution's own arithmetic would appear (Sec. 6.1).
  * Checks every fault as ftcnn_inject does. */
 int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
-                        ftcnn_report *rep, int32_t cap_fixes, const ftcnn_fault *faults, int32_t nf,
-                        void *workspace, hipStream_t stream);
+                        const ftcnn_checksums *ck, ftcnn_report *rep, int32_t cap_fixes,
+                        const ftcnn_fault *faults, int32_t nf, void *workspace, hipStream_t stream);
 
 /* ftcnn_verify_correct over the partial sums that ftcnn_conv_fwd_sums left in
  * the workspace (one launch; O is read only at flagged positions).  The
- * report must be the one ftcnn_conv_fwd_sums reset.  Writes ck->so5, so6,
- * so7, q5 and the flag map; same decisions and repairs as ftcnn_verify_correct. */
+ * report must be the one ftcnn_conv_fwd_sums reset.  which = 0: Co5..Co7 are
+ * read from ck (ftcnn_checksum_conv ran before); which = FTCNN_CO5 |
+ * FTCNN_CO6 | FTCNN_CO7: the same launch computes them from ck->cd1, cd2,
+ * cw1, cw2 at every position first and stores them in ck->co5, co6, co7.
+ * Writes ck->so5, so6, so7, q5 and the flag map; same decisions and repairs
+ * as ftcnn_verify_correct. */
 int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                               const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
-                              void *workspace, hipStream_t stream);
+                              uint32_t which, void *workspace, hipStream_t stream);
 
-/* The whole path of one protected layer on one stream:
- * encode(D) -> conv_fwd_sums -> checksum_conv(CO5|CO6|CO7) -> verify_correct_sums.
- * ck->cw1/cw2 must hold the encoded W (ftcnn_encode with which = 1). */
+/* The whole path of one protected layer on one stream, in two launches:
+ * conv_fwd_sums (with the encode of Cd1, Cd2) -> verify_correct_sums (with
+ * Co5..Co7).  ck->cw1/cw2 must hold the encoded W (ftcnn_encode with
+ * which = 1); ck->cd1, cd2, co5..co7, so5..so7 and q5 are written. */
 int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                          const ftcnn_checksums *ck, const ftcnn_policy *policy,
                          ftcnn_report *rep, int32_t cap_fixes, void *workspace,

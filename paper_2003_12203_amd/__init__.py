@@ -113,16 +113,18 @@ def verify_correct(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
            "ftcnn_verify_correct")
 
 
-def conv_fwd_sums(desc, D, W, O, report, cap, workspace, faults: Sequence[dict] = (), stream=None) -> None:
+def conv_fwd_sums(desc, D, W, O, ck, report, cap, workspace, faults: Sequence[dict] = (), stream=None) -> None:
     arr = _fault_array(faults)
-    _check(lib().ftcnn_conv_fwd_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), _ptr(report), cap,
-                                     arr if faults else None, len(faults), _ptr(workspace), _stream(stream)),
+    _check(lib().ftcnn_conv_fwd_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck) if ck else None,
+                                     _ptr(report), cap, arr if faults else None, len(faults), _ptr(workspace),
+                                     _stream(stream)),
            "ftcnn_conv_fwd_sums")
 
 
-def verify_correct_sums(desc, D, W, O, ck, policy, report, workspace, stream=None) -> None:
+def verify_correct_sums(desc, D, W, O, ck, policy, report, workspace, which: int = 0, stream=None) -> None:
     _check(lib().ftcnn_verify_correct_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck),
-                                           C.byref(policy), _ptr(report), _ptr(workspace), _stream(stream)),
+                                           C.byref(policy), _ptr(report), which, _ptr(workspace),
+                                           _stream(stream)),
            "ftcnn_verify_correct_sums")
 
 
@@ -246,11 +248,18 @@ class Layer:
     def verify_correct(self, D, W, O, stream=None):
         verify_correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace, stream)
 
-    def conv_sums(self, D, W, O, faults=(), stream=None):
-        conv_fwd_sums(self.desc, D, W, O, self.report, self.cap, self.workspace, faults, stream)
+    def conv_sums(self, D, W, O, faults=(), stream=None, encode=False):
+        """ftcnn_conv_fwd_sums; encode=True also encodes Cd1, Cd2 of D in the same launch."""
+        ck = None
+        if encode:
+            ck = _lib.Checksums()
+            ck.cd1, ck.cd2 = self.buf["cd1"].data_ptr(), self.buf["cd2"].data_ptr()
+        conv_fwd_sums(self.desc, D, W, O, ck, self.report, self.cap, self.workspace, faults, stream)
 
-    def verify_correct_sums(self, D, W, O, stream=None):
-        verify_correct_sums(self.desc, D, W, O, self.ck, self.policy, self.report, self.workspace, stream)
+    def verify_correct_sums(self, D, W, O, stream=None, coc=False):
+        """ftcnn_verify_correct_sums; coc=True also computes Co5..Co7 in the same launch."""
+        verify_correct_sums(self.desc, D, W, O, self.ck, self.policy, self.report, self.workspace,
+                            (CO5 | CO6 | CO7) if coc else 0, stream)
 
     def protected(self, D, W, O, stream=None):
         protected_conv(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace,
@@ -264,44 +273,11 @@ class Layer:
         return parse_report(self.report)
 
     def protected_fused(self, D, W, O, faults=(), stream=None):
-        """The protected layer on one stream with the summations in the convolution's epilogue:
-        encode(D) -> conv_fwd_sums -> checksum_conv(Co5, Co6, Co7) -> verify_correct_sums.
+        """The protected layer in two launches (what ftcnn_protected_conv does):
+        conv_fwd_sums with the encode of D -> verify_correct_sums with Co5..Co7.
         ``faults`` (testing) are planted in the convolution's outputs before they are summed."""
-        self.encode_input(D, stream)
-        self.conv_sums(D, W, O, faults, stream)
-        self.checksum_conv(CO5 | CO6 | CO7, stream=stream)
-        self.verify_correct_sums(D, W, O, stream)
-
-    def protected_overlapped(self, D, W, O, side, faults=(), done=None, fused=True):
-        """The protected layer with the input checksums on a second stream.
-
-        encode(D) and checksum_conv(Co5, Co6, Co7) need only D and the weight
-        checksums, so they run on ``side`` while the convolution runs on the
-        current stream; the final detection and correction wait for both.
-        ``done`` (an event the caller records after the previous use of this
-        layer) keeps the next encode from overwriting checksums a pending
-        correction still reads.  fused=True sums O in the convolution's
-        epilogue (faults are planted there); otherwise O is re-read by
-        verify_correct after ``faults`` are injected into it.
-        """
-        main = torch.cuda.current_stream()
-        ready = torch.cuda.Event()
-        with torch.cuda.stream(side):
-            if done is not None:
-                side.wait_event(done)
-            self.encode_input(D, side)
-            self.checksum_conv(CO5 | CO6 | CO7, stream=side)
-            ready.record(side)
-        if fused:
-            self.conv_sums(D, W, O, faults, main)
-            main.wait_event(ready)
-            self.verify_correct_sums(D, W, O, main)
-            return
-        self.conv(D, W, O, main)
-        if faults:
-            self.inject(O, faults, main)
-        main.wait_event(ready)
-        self.verify_correct(D, W, O, main)
+        self.conv_sums(D, W, O, faults, stream, encode=True)
+        self.verify_correct_sums(D, W, O, stream, coc=True)
 
     def run(self, D, W, O, faults=(), stream=None) -> Report:
         """The full workflow of Sec. 4.3 with recomputation of the layer when needed (Sec. 4.1.1)."""

@@ -92,9 +92,11 @@ def load(path: str = LIB_PATH):
     L.ftcnn_verify_correct.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp, C.c_int32,
                                        _dp, _dp]
     L.ftcnn_verify_correct.restype = C.c_int
-    L.ftcnn_conv_fwd_sums.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, C.c_int32, P(Fault), C.c_int32, _dp, _dp]
+    L.ftcnn_conv_fwd_sums.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), _dp, C.c_int32, P(Fault),
+                                      C.c_int32, _dp, _dp]
     L.ftcnn_conv_fwd_sums.restype = C.c_int
-    L.ftcnn_verify_correct_sums.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp, _dp, _dp]
+    L.ftcnn_verify_correct_sums.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp,
+                                            C.c_uint32, _dp, _dp]
     L.ftcnn_verify_correct_sums.restype = C.c_int
     L.ftcnn_protected_conv.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp,
                                        C.c_int32, _dp, _dp]

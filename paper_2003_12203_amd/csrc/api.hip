@@ -83,14 +83,10 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     if (pl->ver_splits > part_cap) pl->ver_splits = part_cap > 1 ? (int)part_cap : 1;
     // summations fused into the convolution epilogue: one slice per (filter tile, image)
     pl->sum_splits = (int)(ceil_div(g.M, conv_tile_m(g)) * g.N);
-    // correction: one scratch slice per workgroup of the widest final detection stage
+    // correction: the standalone launch has corr_blocks workgroups, one scratch slice each; in
+    // the fused final stage a workgroup with flagged positions takes the next free slice
     pl->corr_blocks = 256;
-    {
-        const int tpp = final_tpp(pl->ver_splits) < final_tpp(pl->sum_splits) ? final_tpp(pl->ver_splits)
-                                                                               : final_tpp(pl->sum_splits);
-        const long long fblocks = ceil_div(EF, kThreads / tpp);
-        pl->corr_slots = (int)(fblocks > pl->corr_blocks ? fblocks : pl->corr_blocks);
-    }
+    pl->corr_slots = 256;
     const long long L = g.M > g.N ? g.M : g.N;
     pl->corr_stride = (size_t)((4LL * g.M + 4LL * g.N + 2 * L + 31) / 32 * 32);
 
@@ -216,26 +212,31 @@ int check_faults(const Geom &g, const ftcnn_fault *faults, int nf, const char *w
     return FTCNN_OK;
 }
 
-int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, ftcnn_report *rep, int32_t cap,
-                 const ftcnn_fault *faults, int32_t nf, void *ws, hipStream_t st) {
+int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
+                 ftcnn_report *rep, int32_t cap, const ftcnn_fault *faults, int32_t nf, void *ws, hipStream_t st) {
     if (!D || !W || !O || !rep) return fail(FTCNN_E_ARG, "conv_fwd_sums: null pointer");
     if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
+    double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
+    if ((cd1 == nullptr) != (cd2 == nullptr)) return fail(FTCNN_E_ARG, "conv_fwd_sums: cd1 and cd2 go together");
     FT_TRY(check_faults(pl.g, faults, nf, "conv_fwd_sums"));
     FT_TRY(check_ws(pl, ws));
-    FT_HIP(launch_conv_sums(pl, D, W, O, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
+    FT_HIP(launch_conv_sums(pl, D, W, O, cd1, cd2, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
     return FTCNN_OK;
 }
 
 int do_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
-                           const ftcnn_policy *pol, ftcnn_report *rep, void *ws, hipStream_t st) {
+                           const ftcnn_policy *pol, ftcnn_report *rep, uint32_t which, void *ws, hipStream_t st) {
     FT_TRY(check_policy(pol));
     if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "verify_correct_sums: null pointer");
+    const uint32_t coc = FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7;
+    if (which != 0 && which != coc)
+        return fail(FTCNN_E_ARG, "verify_correct_sums: which must be 0 or CO5|CO6|CO7 (0x%x)", which);
     if (!ck->co5 || !ck->so5 || !ck->so6 || !ck->so7 || !ck->q5)
         return fail(FTCNN_E_ARG, "verify needs co5, so5, so6, so7 and q5");
     if (!ck->cd1 || !ck->cd2 || !ck->cw1 || !ck->cw2 || !ck->co6 || !ck->co7)
         return fail(FTCNN_E_ARG, "correct needs cd1, cd2, cw1, cw2, co5, co6 and co7");
     FT_TRY(check_ws(pl, ws));
-    FT_HIP(launch_verify_correct_sums(pl, D, W, O, *ck, *pol, rep, ws, st), "verify_correct_sums");
+    FT_HIP(launch_verify_correct_sums(pl, D, W, O, *ck, *pol, rep, which == coc, ws, st), "verify_correct_sums");
     return FTCNN_OK;
 }
 
@@ -321,26 +322,26 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
     FT_TRY(check_policy(policy));
     if (!ck || !D || !W || !O || !rep) return fail(FTCNN_E_ARG, "protected_conv: null pointer");
     FT_TRY(check_ws(pl, workspace));
-    FT_TRY(do_encode(pl, 0, D, ck->cd1, ck->cd2, workspace, stream));
-    FT_TRY(do_conv_sums(pl, D, W, O, rep, cap_fixes, nullptr, 0, workspace, stream));
-    FT_TRY(do_cksum(pl, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, D, W, ck, stream));
-    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, workspace, stream);
+    if (!ck->cd1 || !ck->cd2) return fail(FTCNN_E_ARG, "protected_conv needs cd1 and cd2");
+    FT_TRY(do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, nullptr, 0, workspace, stream));
+    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, workspace,
+                                  stream);
 }
 
-int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O, ftcnn_report *rep,
-                        int32_t cap_fixes, const ftcnn_fault *faults, int32_t nf, void *workspace,
-                        hipStream_t stream) {
+int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                        const ftcnn_checksums *ck, ftcnn_report *rep, int32_t cap_fixes, const ftcnn_fault *faults,
+                        int32_t nf, void *workspace, hipStream_t stream) {
     Plan pl;
     FT_TRY(make_plan(desc, &pl));
-    return do_conv_sums(pl, D, W, O, rep, cap_fixes, faults, nf, workspace, stream);
+    return do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, faults, nf, workspace, stream);
 }
 
 int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                               const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
-                              void *workspace, hipStream_t stream) {
+                              uint32_t which, void *workspace, hipStream_t stream) {
     Plan pl;
     FT_TRY(make_plan(desc, &pl));
-    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, workspace, stream);
+    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, which, workspace, stream);
 }
 
 int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,

@@ -327,14 +327,79 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
 // rows give sum O, sum (m + wbase) O, (n + wbase) sum O and sum O^2, written as
 // slice (tile_m * N + n) of a [slices][4][E*F] float64 array; block 0 resets the
 // report.  EPI 2: EPI 1 with faults planted in the stored values first.
+// With EPI 1 and 2 the grid may also carry enc_blocks leading workgroups that
+// encode the input checksums Cd1, Cd2 of D (Sec. 3.2) instead of a tile: that
+// memory-bound work then runs beside the matrix-bound tiles of the same launch.
 struct NoFaults {};
+constexpr int kEncVec = 4;   // columns per thread in the encode workgroups
 template <int EPI> struct Epi {
     double *part;
     ftcnn_report *rep;
     int cap;
+    double *cd1, *cd2;
+    int enc_blocks;   // a multiple of 8, so tiles keep their XCD assignment
+    int enc_vec;      // 16-byte loads in the encode blocks
     typename std::conditional<EPI == 2, FaultList, NoFaults>::type fl;
 };
 template <> struct Epi<0> {};
+
+// V elements of one row of D, loaded as one unit (V * sizeof(T) is 2 to 16 bytes).
+template <typename T, int V> union RowPack {
+    using Q = typename std::conditional<
+        V * sizeof(T) == 16, uint4,
+        typename std::conditional<V * sizeof(T) == 8, uint2,
+                                  typename std::conditional<V * sizeof(T) == 4, uint32_t, uint16_t>::type>::type>::type;
+    Q q;
+    T e[V];
+};
+
+// One encode workgroup: V consecutive columns of D viewed as [N][Ch*H*W] per
+// thread, every row n in order (eight rows of loads in flight), accumulated in
+// float64: Cd1 = sum_n D_n and Cd2 = sum_n (n + wbase) D_n.
+template <typename T, int NT, int V>
+__device__ void encode_block(const T *__restrict__ D, const Geom &g, int blk, double *__restrict__ cd1,
+                             double *__restrict__ cd2) {
+    const long long col = ((long long)blk * NT + threadIdx.x) * V;
+    if (col >= g.CHW) return;
+    const int nv = (long long)V <= g.CHW - col ? V : (int)(g.CHW - col);   // V == 1 whenever Ch*H*W % V != 0
+    double a1[V], a2[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) a1[e] = a2[e] = 0.0;
+    const T *src = D + col;
+    // rows stay packed in registers until they are added (V elements per row in flight)
+    using P = RowPack<T, V>;
+    auto load = [&](long long row) -> P {
+        P pk;
+        pk.q = *reinterpret_cast<const typename P::Q *>(src + row * g.CHW);
+        return pk;
+    };
+    auto add = [&](const P &pk, int n) {
+        const double w = (double)(n + g.wbase);
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            double x;
+            if constexpr (sizeof(T) == 4) x = (double)pk.e[e];
+            else x = (double)bf16_bits_to_f32(pk.e[e]);
+            a1[e] += x;
+            a2[e] = fma(w, x, a2[e]);
+        }
+    };
+    int n = 0;
+    for (; n + 7 < g.N; n += 8) {
+        P v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = load(n + u);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) add(v[u], n + u);
+    }
+    for (; n < g.N; ++n) add(load(n), n);
+#pragma unroll
+    for (int e = 0; e < V; ++e)
+        if (e < nv) {
+            cd1[col + e] = a1[e];
+            cd2[col + e] = a2[e];
+        }
+}
 
 template <typename T> struct Bits;
 template <> struct Bits<float> {
@@ -361,12 +426,22 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     T *Bs0 = As0 + 2 * C::TM * C::LDK;
 
     const int tid = threadIdx.x;
+    int bid = blockIdx.x;
+    if constexpr (EPI != 0) {
+        if (bid == 0 && tid == 0) reset_report(ep.rep, ep.cap);
+        if (bid < ep.enc_blocks) {
+            if (ep.enc_vec) encode_block<T, C::NT, kEncVec>(D, g, bid, ep.cd1, ep.cd2);
+            else encode_block<T, C::NT, 1>(D, g, bid, ep.cd1, ep.cd2);
+            return;
+        }
+        bid -= ep.enc_blocks;
+    }
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wp = wave / WM;
     // logical tile order: pixel-major keeps the M tiles of one pixel tile on one
     // XCD (its L2 serves the repeated D reads); M-major keeps one slab of W
     // resident per XCD instead (preferred when W is larger than an XCD's L2)
-    const int tile = xcd_tile(blockIdx.x, tiles_total);
+    const int tile = xcd_tile(bid, tiles_total);
     const int tiles_p = tiles_total / tiles_m;
     const int mt = m_major ? tile / tiles_p : tile % tiles_m;
     const int pt = m_major ? tile % tiles_p : tile / tiles_m;
@@ -468,7 +543,6 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         }
     } else {
         using Bt = Bits<T>;
-        if (blockIdx.x == 0 && tid == 0) reset_report(ep.rep, ep.cap);
         // faults inside this tile (a uniform test; usually none)
         bool planted = false;
         if constexpr (EPI == 2) {
@@ -582,15 +656,26 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     const int tiles_m = (g.M + C::TM - 1) / C::TM;
     const long long tiles_p = (g.P_total + C::TP - 1) / C::TP;
     const long long total = tiles_p * tiles_m;
-    if (total > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    Epi<EPI> e = ep;
+    long long enc = 0;
+    if constexpr (EPI != 0) {
+        if (e.cd1) {
+            e.enc_vec = g.CHW % kEncVec == 0 && reinterpret_cast<uintptr_t>(D) % (kEncVec * sizeof(T)) == 0;
+            const long long per = (long long)C::NT * (e.enc_vec ? kEncVec : 1);
+            enc = ((g.CHW + per - 1) / per + 7) / 8 * 8;
+        }
+        e.enc_blocks = (int)enc;
+    }
+    if (total + enc > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI>;
     if constexpr (C::LDS_BYTES > 65536) {
         static const hipError_t attr = hipFuncSetAttribute(
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
         if (attr != hipSuccess) return attr;
     }
-    kern<<<(unsigned)total, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D), static_cast<const T *>(W),
-                                                       static_cast<T *>(O), g, tiles_m, (int)total, m_major, ep);
+    kern<<<(unsigned)(total + enc), C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D),
+                                                               static_cast<const T *>(W), static_cast<T *>(O), g,
+                                                               tiles_m, (int)total, m_major, e);
     return hipGetLastError();
 }
 
@@ -653,14 +738,15 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
     return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
-hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, ftcnn_report *rep, int cap,
-                            const ftcnn_fault *faults, int nf, void *ws, hipStream_t st) {
+hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, double *cd1, double *cd2,
+                            ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
+                            hipStream_t st) {
     double *part = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_sums);
     if (nf == 0) {
-        Epi<1> ep{part, rep, cap, {}};
+        Epi<1> ep{part, rep, cap, cd1, cd2, 0, 0, {}};
         return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
     }
-    Epi<2> ep{part, rep, cap, {}};
+    Epi<2> ep{part, rep, cap, cd1, cd2, 0, 0, {}};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
     return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });

@@ -34,7 +34,8 @@ struct Sh {
     int off[KC];
     int flagbuf[kThreads];
     int list[kThreads];
-    int nlist;
+    double colist[kThreads][3];   // Co5, Co6, Co7 of the listed positions
+    int nlist, slot;
     int nfix, fail, cnt_m, cnt_n, one_m, one_n;
     double bcast[4];
 };
@@ -541,9 +542,9 @@ template <typename T> __device__ void record(const Ctx<T> &c, Sh &sh, int scheme
     __syncthreads();
 }
 
-template <typename T> __device__ void resolve(const Ctx<T> &c, Sh &sh, int p) {
+template <typename T> __device__ void resolve(const Ctx<T> &c, Sh &sh, int p, const double (&co_in)[3]) {
     const int x = p / c.g.F, y = p - (p / c.g.F) * c.g.F;
-    double co[3] = {c.co5g[p], c.co6g[p], c.co7g[p]};
+    double co[3] = {co_in[0], co_in[1], co_in[2]};
     double s[6];
     sums6(c, p, sh, s);
     double d[3] = {co[0] - s[0], co[1] - s[1], co[2] - s[2]};
@@ -614,27 +615,67 @@ __global__ __launch_bounds__(kThreads) void correct_kernel(Ctx<T> c, const int *
         }
         __syncthreads();
         const int cnt = sh.nlist;
-        for (int i = 0; i < cnt; ++i) resolve(c, sh, sh.list[i]);
+        for (int i = 0; i < cnt; ++i) {
+            const int p = sh.list[i];
+            const double co[3] = {c.co5g[p], c.co6g[p], c.co7g[p]};
+            resolve(c, sh, p, co);
+        }
         __syncthreads();
+    }
+}
+
+// Co5 = Cd1 (x) Cw1, Co6 = Cd1 (x) Cw2, Co7 = Cd2 (x) Cw1 at position (x, y)
+// (Sec. 3.2): this lane's share of the K taps, k = lane, lane + TPP, ...,
+// with (ch, r, s) advanced incrementally.
+template <typename T, int TPP>
+__device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double &c5, double &c6, double &c7) {
+    const Geom &g = c.g;
+    const int RS = g.R * g.S;
+    int ch = lane / RS, rem = lane - ch * RS;
+    int r = rem / g.S, s = rem - r * g.S;
+    const int dch = TPP / RS, drem = TPP - dch * RS, dr = drem / g.S, ds = drem - dr * g.S;
+    const int ih0 = g.U * x - g.P, iw0 = g.U * y - g.P;
+    for (int k = lane; k < g.K; k += TPP) {
+        const int ih = ih0 + r, iw = iw0 + s;
+        if ((unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W) {
+            const long long off = ((long long)ch * g.H + ih) * g.W + iw;
+            const double d1 = c.cd1[off], d2 = c.cd2[off];
+            const double w1 = c.cw1[k], w2 = c.cw2[k];
+            c5 = fma(d1, w1, c5);
+            c6 = fma(d1, w2, c6);
+            c7 = fma(d2, w1, c7);
+        }
+        s += ds;
+        r += dr;
+        ch += dch;
+        if (s >= g.S) { s -= g.S; ++r; }
+        if (r >= g.R) { r -= g.R; ++ch; }
     }
 }
 
 // Final stage of the detection (the split partials of each position summed in a
 // fixed order, then the CoC-D test) with the correction chain run in the same
 // workgroup for every position it flags.  A clean layer pays nothing for the
-// correction module, and no separate launch is needed.
-template <typename T, int TPP>
+// correction module, and no separate launch is needed.  With COC the same
+// lanes first compute Co5..Co7 of their position and store them.
+template <typename T, int TPP, bool COC>
 __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int splits, const double *__restrict__ part,
+                                                                  double *co5, double *co6, double *co7,
                                                                   double *so5, double *so6, double *so7, double *q5,
                                                                   int *__restrict__ flags, double *scratch,
-                                                                  size_t stride) {
+                                                                  size_t stride, int nslots) {
     __shared__ Sh sh;
     const Geom &g = c.g;
     const int per = kThreads / TPP;
     const int lane = threadIdx.x % TPP, slot = threadIdx.x / TPP;
     const int p = blockIdx.x * per + slot;
+    double c5 = 0.0, c6 = 0.0, c7 = 0.0;
     double a = 0.0, b = 0.0, cc = 0.0, d = 0.0;
     if (p < g.EF) {
+        if constexpr (COC) {
+            const int x = p / g.F;
+            coc_taps<T, TPP>(c, lane, x, p - x * g.F, c5, c6, c7);
+        }
         for (int s = lane; s < splits; s += TPP) {
             const double *ps = part + (size_t)s * 4 * g.EF + p;
             a += ps[0];
@@ -643,38 +684,89 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
             d += ps[3 * (size_t)g.EF];
         }
     }
+    if constexpr (TPP == kThreads) {
+        // one position per workgroup: waves first, then the four waves in order
+        if constexpr (COC) {
+            double v[7] = {a, b, cc, d, c5, c6, c7};
+            bsum<7>(v, sh);
+            a = v[0]; b = v[1]; cc = v[2]; d = v[3]; c5 = v[4]; c6 = v[5]; c7 = v[6];
+        } else {
+            double v[4] = {a, b, cc, d};
+            bsum<4>(v, sh);
+            a = v[0]; b = v[1]; cc = v[2]; d = v[3];
+        }
+    } else {
 #pragma unroll
-    for (int o = TPP / 2; o > 0; o >>= 1) {
-        a += __shfl_xor(a, o, 64);
-        b += __shfl_xor(b, o, 64);
-        cc += __shfl_xor(cc, o, 64);
-        d += __shfl_xor(d, o, 64);
+        for (int o = TPP / 2; o > 0; o >>= 1) {
+            a += __shfl_xor(a, o, 64);
+            b += __shfl_xor(b, o, 64);
+            cc += __shfl_xor(cc, o, 64);
+            d += __shfl_xor(d, o, 64);
+            if constexpr (COC) {
+                c5 += __shfl_xor(c5, o, 64);
+                c6 += __shfl_xor(c6, o, 64);
+                c7 += __shfl_xor(c7, o, 64);
+            }
+        }
     }
     int flag = 0;
     if (p < g.EF && lane == 0) {
+        if constexpr (COC) {
+            co5[p] = c5;
+            co6[p] = c6;
+            co7[p] = c7;
+        } else {
+            c5 = c.co5g[p];
+            c6 = c.co6g[p];
+            c7 = c.co7g[p];
+        }
         const double q = sqrt(d);
         so5[p] = a;
         so6[p] = b;
         so7[p] = cc;
         q5[p] = q;
-        flag = is_bad(c.co5g[p] - a, q, c.scale) ? 1 : 0;
+        flag = is_bad(c5 - a, q, c.scale) ? 1 : 0;
         flags[p] = flag;
         sh.flagbuf[slot] = flag;
+        sh.colist[slot][0] = c5;
+        sh.colist[slot][1] = c6;
+        sh.colist[slot][2] = c7;
     }
     const int cnt = __syncthreads_count(flag);
     if (cnt == 0) return;
     if (threadIdx.x == 0) {
         atomicAdd(&c.rep->n_flagged, cnt);
         atomicMax(&c.rep->detected, 1);
+        // compact the flagged slots in place (slot t moves to n <= t)
         int n = 0;
         for (int t = 0; t < per; ++t)
-            if (blockIdx.x * per + t < g.EF && sh.flagbuf[t]) sh.list[n++] = blockIdx.x * per + t;
+            if (blockIdx.x * per + t < g.EF && sh.flagbuf[t]) {
+                sh.list[n] = blockIdx.x * per + t;
+                sh.colist[n][0] = sh.colist[t][0];
+                sh.colist[n][1] = sh.colist[t][1];
+                sh.colist[n][2] = sh.colist[t][2];
+                ++n;
+            }
         sh.nlist = n;
+        // a scratch slice for this workgroup's chain, taken from the report's slot counter
+        sh.slot = atomicAdd(&c.rep->reserved[0], 1);
     }
     __syncthreads();
-    bind_scratch(c, scratch + stride * blockIdx.x);
     const int nl = sh.nlist;
-    for (int i = 0; i < nl; ++i) resolve(c, sh, sh.list[i]);
+    if (sh.slot >= nslots) {
+        // more flagged workgroups than scratch slices: leave these positions to recomputation
+        for (int i = 0; i < nl; ++i) {
+            begin_scheme<T>(sh);
+            const int p = sh.list[i];
+            record(c, sh, FTCNN_SCHEME_UNRESOLVED, p / g.F, p - (p / g.F) * g.F);
+        }
+        return;
+    }
+    bind_scratch(c, scratch + stride * sh.slot);
+    for (int i = 0; i < nl; ++i) {
+        const double co[3] = {sh.colist[i][0], sh.colist[i][1], sh.colist[i][2]};
+        resolve(c, sh, sh.list[i], co);
+    }
 }
 
 template <typename T>
@@ -699,22 +791,32 @@ Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftc
 
 template <typename T>
 hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums &ck,
-                     const ftcnn_policy &pol, ftcnn_report *rep, void *ws, size_t off_part, int sp,
+                     const ftcnn_policy &pol, ftcnn_report *rep, void *ws, size_t off_part, int sp, bool coc,
                      hipStream_t st) {
     const Ctx<T> c = make_ctx<T>(pl, D, W, O, ck, pol, rep);
     char *w = static_cast<char *>(ws);
     const double *part = reinterpret_cast<const double *>(w + off_part);
     int *flags = reinterpret_cast<int *>(w + pl.off_flags);
     double *scratch = reinterpret_cast<double *>(w + pl.off_corr);
-    const int tpp = final_tpp(sp);
+    const int tpp = final_tpp(sp, coc ? pl.g.K : 0);
     const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
-#define VC(TPP)                                                                                          \
-    verify_correct_kernel<T, TPP><<<blocks, kThreads, 0, st>>>(c, sp, part, ck.so5, ck.so6, ck.so7, ck.q5, \
-                                                               flags, scratch, pl.corr_stride)
-    if (tpp == 1) VC(1);
-    else if (tpp == 4) VC(4);
-    else if (tpp == 16) VC(16);
-    else VC(64);
+#define VC(TPP, COC)                                                                                       \
+    verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, ck.co5, ck.co6, ck.co7,   \
+                                                                    ck.so5, ck.so6, ck.so7, ck.q5, flags,   \
+                                                                    scratch, pl.corr_stride, pl.corr_slots)
+    if (coc) {
+        if (tpp == 1) VC(1, true);
+        else if (tpp == 4) VC(4, true);
+        else if (tpp == 16) VC(16, true);
+        else if (tpp == 64) VC(64, true);
+        else VC(kThreads, true);
+    } else {
+        if (tpp == 1) VC(1, false);
+        else if (tpp == 4) VC(4, false);
+        else if (tpp == 16) VC(16, false);
+        else if (tpp == 64) VC(64, false);
+        else VC(kThreads, false);
+    }
 #undef VC
     return hipGetLastError();
 }
@@ -759,16 +861,17 @@ hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, v
                                  int cap, void *ws, hipStream_t st) {
     hipError_t e = launch_verify_partial(pl, O, rep, cap, ws, st);
     if (e != hipSuccess) return e;
-    if (pl.g.dtype == FTCNN_F32) return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, st);
-    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, st);
+    if (pl.g.dtype == FTCNN_F32)
+        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, false, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, false, st);
 }
 
 hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O,
                                       const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
-                                      void *ws, hipStream_t st) {
+                                      bool coc, void *ws, hipStream_t st) {
     if (pl.g.dtype == FTCNN_F32)
-        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, st);
-    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, st);
+        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, coc, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, coc, st);
 }
 
 }  // namespace ftcnn

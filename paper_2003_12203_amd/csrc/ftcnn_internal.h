@@ -113,10 +113,12 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
 // The convolution with the CoC-D summations in its epilogue: every tile also
 // writes its (So5, So6, So7, sum of squares) partials for the pixels it owns to
 // the workspace (pl.sum_splits slices, layout of the verification partials) and
-// the report is reset.  faults (at most kMaxFaults, host array) are planted in
-// the stored values before they are summed.
-hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, ftcnn_report *rep, int cap,
-                            const ftcnn_fault *faults, int nf, void *ws, hipStream_t st);
+// the report is reset.  With cd1 and cd2 set, extra workgroups of the same
+// launch encode Cd1, Cd2 of D.  faults (at most kMaxFaults, host array) are
+// planted in the stored values before they are summed.
+hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, double *cd1, double *cd2,
+                            ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
+                            hipStream_t st);
 // Rows of C per workgroup tile of the convolution chosen for this layer.
 int conv_tile_m(const Geom &g);
 hipError_t launch_checksum_conv(const Plan &pl, uint32_t which, const void *D, const void *W,
@@ -132,14 +134,19 @@ hipError_t launch_verify_partial(const Plan &pl, const void *O, ftcnn_report *re
 hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, void *O,
                                  const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
                                  int cap, void *ws, hipStream_t st);
-// Final detection stage and correction over the partials the convolution epilogue wrote.
+// Final detection stage and correction over the partials the convolution epilogue wrote;
+// with coc, Co5..Co7 are computed in the same launch from Cd1, Cd2, Cw1, Cw2.
 hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O,
                                       const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
-                                      void *ws, hipStream_t st);
+                                      bool coc, void *ws, hipStream_t st);
 
 // Threads that share one position in the final verification stage (a power of
-// two; the float64 split partials of that position are spread over them).
-inline int final_tpp(int splits) { return splits <= 1 ? 1 : splits <= 4 ? 4 : splits <= 16 ? 16 : 64; }
+// two; the float64 split partials of that position, and the K taps of its
+// Co5..Co7 when those are computed there too, are spread over them).
+inline int final_tpp(int splits, int taps = 0) {
+    const int w = splits > taps / 4 ? splits : taps / 4;
+    return w <= 1 ? 1 : w <= 4 ? 4 : w <= 16 ? 16 : w <= 128 ? 64 : kThreads;
+}
 hipError_t launch_inject(const Plan &pl, void *O, const ftcnn_fault *f, int nf, hipStream_t st);
 
 }  // namespace ftcnn

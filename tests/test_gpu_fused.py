@@ -5,6 +5,9 @@ separate kernels and the oracle.
 * So5, So6, So7 and Q5 from the epilogue partials agree with the oracle's summations of the
   GPU's own output (Sec. 3.6) to float64 rounding, and exactly on integer data;
 * faults planted in the epilogue give bitwise the output that ftcnn_inject gives afterwards;
+* the two-launch path (input checksums encoded by extra workgroups of the convolution launch,
+  Co5..Co7 computed in the final launch) gives the checksums of the separate kernels and the
+  oracle;
 * ftcnn_protected_conv (the whole path in one call) matches the step-by-step path.
 """
 import numpy as np
@@ -53,6 +56,35 @@ def test_epilogue_sums_match_oracle(cfg, li, spec, wbase):
     assert not rep.detected and rep.status == ft.STATUS_CLEAN and rep.n_flagged == 0
 
 
+@pytest.mark.parametrize("cfg,li,spec", workload_shapes())
+def test_two_launch_checksums_match_oracle(cfg, li, spec):
+    D, W = wl.gen_d(cfg, li, spec), wl.gen_w(cfg, li, spec)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
+    lay.encode_weights(Wd)
+    O_ref = lay.empty_output()
+    lay.conv(Dd, Wd, O_ref)
+    O = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O, encode=True)
+    lay.verify_correct_sums(Dd, Wd, O, coc=True)
+    torch.cuda.synchronize()
+    iv = torch.int16 if spec.dtype == "bf16" else torch.int32
+    assert torch.equal(O.view(iv), O_ref.view(iv)), "O differs from conv_fwd"
+    b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
+    cd1, cd2 = wf.encode(D, 0)
+    np.testing.assert_allclose(b["cd1"], cd1.ravel(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(b["cd2"], cd2.ravel(), rtol=1e-12, atol=1e-10)
+    ck = wf.Checksums(cd1, cd2, *wf.encode(W, 0))
+    wf.coc_checksums(ck, spec.stride, spec.pad)
+    for name, ref in [("co5", ck.co5), ("co6", ck.co6), ("co7", ck.co7)]:
+        assert_close_scaled(b[name].reshape(ref.shape), ref, 1e-11, name)
+    so5, so6, so7, q5, flags = wf.verify(host(O), ck.co5, spec.ch * spec.r * spec.s, spec.dtype, wf.Policy())
+    for name, ref in [("so5", so5), ("so6", so6), ("so7", so7), ("q5", q5)]:
+        assert_close_scaled(b[name].reshape(ref.shape), ref, 1e-11, name)
+    assert not flags.any() and not gpu_flags(lay).any()
+    assert not lay.read_report().detected
+
+
 @pytest.mark.parametrize("shape", [
     # n, ch, h, m, r, stride, pad: ragged pixel tails, partial filter tiles, several tiles per image
     (5, 6, 12, 9, 3, 1, 1),
@@ -72,13 +104,14 @@ def test_epilogue_sums_integer_exact(shape, dtype):
     lay = layer_for(spec)
     Dd, Wd = dev(D, dtype), dev(W, dtype)
     lay.encode_weights(Wd)
-    lay.encode_input(Dd)
     O = lay.empty_output()
-    lay.conv_sums(Dd, Wd, O)
-    lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
-    lay.verify_correct_sums(Dd, Wd, O)
+    lay.conv_sums(Dd, Wd, O, encode=True)
+    lay.verify_correct_sums(Dd, Wd, O, coc=True)
     torch.cuda.synchronize()
     b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
+    cd1, cd2 = wf.encode(D, 0)
+    np.testing.assert_array_equal(b["cd1"], cd1.ravel())
+    np.testing.assert_array_equal(b["cd2"], cd2.ravel())
     if dtype == "f32" or np.abs(host(O)).max() <= 256:
         np.testing.assert_array_equal(b["co5"], b["so5"])
         np.testing.assert_array_equal(b["co6"], b["so6"])

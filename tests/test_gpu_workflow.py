@@ -5,7 +5,10 @@ Every case runs through each of the library's detection paths:
 * ``separate``: ftcnn_verify then ftcnn_correct, faults injected into the stored O;
 * ``fused``: ftcnn_verify_correct (one detection read of O, correction in the same launch);
 * ``epilogue``: ftcnn_conv_fwd_sums (summations in the convolution's epilogue, faults planted
-  in its outputs before they are summed) then ftcnn_verify_correct_sums.
+  in its outputs before they are summed) then ftcnn_verify_correct_sums;
+* ``two_launch``: the same with the input checksums encoded inside the convolution launch and
+  Co5..Co7 computed inside the final launch (ftcnn_protected_conv).  Cases that corrupt D or a
+  checksum between the encode and the convolution do not apply to it.
 
 Decisions are compared in decision-oracle mode: the oracle's workflow runs on
 the GPU's own faulted output (before correction), so only the float64 order of
@@ -36,7 +39,7 @@ def _flat(spec, target, index):
     return (c * spec.r + r) * spec.s + s
 
 
-MODES = ["separate", "fused", "epilogue"]
+MODES = ["separate", "fused", "epilogue", "two_launch"]
 
 
 def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None, mode="separate"):
@@ -44,7 +47,10 @@ def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None, mode="separate"):
     lay = layer_for(spec, wbase=wbase, **pol_kw)
     Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
     lay.encode_weights(Wd)
-    lay.encode_input(Dd)
+    if mode == "two_launch":
+        assert hook is None, "no point between encode and convolution in the two-launch path"
+    else:
+        lay.encode_input(Dd)
     if hook is not None:
         t = hook["target"]
         if t == "D":
@@ -54,7 +60,11 @@ def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None, mode="separate"):
         else:
             lay.buf[t][_flat(spec, t, hook["index"])] += hook["add"]
     O = lay.empty_output()
-    if mode == "epilogue":
+    if mode == "two_launch":
+        lay.conv_sums(Dd, Wd, O, to_ft_faults(faults), encode=True)
+        O_faulty = host(O)
+        lay.verify_correct_sums(Dd, Wd, O, coc=True)
+    elif mode == "epilogue":
         lay.conv_sums(Dd, Wd, O, to_ft_faults(faults))
         O_faulty = host(O)
         lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
@@ -74,7 +84,10 @@ def run_gpu(spec, D, W, faults, pol_kw, wbase=0, hook=None, mode="separate"):
     flags = gpu_flags(lay)
     status = rep.status
     if status == ft.STATUS_NEEDS_RECOMPUTE:
-        if mode == "epilogue":
+        if mode == "two_launch":
+            lay.conv_sums(Dd, Wd, O, encode=True)
+            lay.verify_correct_sums(Dd, Wd, O, coc=True)
+        elif mode == "epilogue":
             lay.conv_sums(Dd, Wd, O)
             lay.verify_correct_sums(Dd, Wd, O)
         else:
@@ -103,6 +116,8 @@ def compare(spec, D, W, rep, status, O_faulty, O_final, flags, policy, hook_fn=N
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("scn", SCN, ids=[s.name for s in SCN])
 def test_scenario_matches_oracle(scn, mode):
+    if mode == "two_launch" and scn.hook is not None:
+        pytest.skip("corrupts D or a checksum between the encode and the convolution")
     D, W = scn.inputs()
     pol = scn.oracle_policy()
     kw = dict(rc_on=pol.rc_on, clc_on=pol.clc_on, repair=pol.repair, kappa=pol.kappa, eta=pol.eta)
@@ -172,7 +187,7 @@ def _pattern_faults(O, draws, count):
     return out
 
 
-@pytest.mark.parametrize("mode", ["fused", "epilogue"])
+@pytest.mark.parametrize("mode", ["fused", "epilogue", "two_launch"])
 @pytest.mark.parametrize("li", [1, 5, 13, 14])
 def test_darknet_multi_fault(li, mode):
     """Darknet-shaped layers (reduced batch and size) with seeded multi-fault injection."""
