@@ -35,7 +35,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-MFMA_PEAK_F32 = 157.3   # TFLOP/s, MI355X dense fp32 matrix
+MFMA_PEAK = {"f32": 157.3, "bf16": 2516.6}   # TFLOP/s, MI355X dense matrix peaks
 FAULT_VALUE = 100.0     # additive corruption, about 120x the rms of these outputs
 
 
@@ -47,6 +47,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="lower bound on the CPU oracle's timed work (whole batch-64 passes)")
+    ap.add_argument("--workload", default="alexnet",
+                    choices=["alexnet", "vgg19", "vgg19_bf16", "resnet18", "darknet19"],
+                    help="layer stack to time (the default is the benchmark's workload; the others report "
+                         "the same figures for the remaining configurations)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run a plain fp32 device copy of this size first (counter calibration)")
     ap.add_argument("--quiet", action="store_true")
@@ -60,8 +64,9 @@ class LayerRun:
         self.name = spec.name
         self.lay = ft.Layer(spec.n, spec.ch, spec.h, spec.w, spec.m, spec.r, spec.s, spec.stride,
                             spec.pad, spec.dtype)
-        self.D = torch.from_numpy(wl.gen_d(cfg, li)).cuda()
-        self.W = torch.from_numpy(wl.gen_w(cfg, li)).cuda()
+        tdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32   # bf16 draws are exact in bf16
+        self.D = torch.from_numpy(wl.gen_d(cfg, li)).to(tdt).cuda()
+        self.W = torch.from_numpy(wl.gen_w(cfg, li)).to(tdt).cuda()
         self.O = self.lay.empty_output()
         self.lay.encode_weights(self.W)
         E, F = self.lay.E, self.lay.F
@@ -86,8 +91,11 @@ def main():
 
     ft.lib()  # fails loudly if the HIP library is missing
     torch.cuda.set_device(0)
-    cfg = wl.config(1)
+    cfg = {"alexnet": wl.config(1), "vgg19": wl.config(2), "vgg19_bf16": wl.vgg19_bf16(),
+           "resnet18": wl.config(3), "darknet19": wl.config(4)}[args.workload]
     runs = [LayerRun(cfg, li, ft, torch) for li in range(len(cfg.layers))]
+    dtype = cfg.layers[0].dtype
+    peak = MFMA_PEAK[dtype]
     nl = len(runs)
     total_flops = sum(r.flops for r in runs)
     torch.cuda.synchronize()
@@ -220,15 +228,17 @@ def main():
     dom_flops = runs[dom].flops
     dom_ms = float(np.mean(dom_conv_ms))
     achieved = dom_flops / (dom_ms * 1e-3) / 1e12
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_PEAK_F32, "unit": "TFLOP/s",
-                "frac": round(achieved / MFMA_PEAK_F32, 4), "traffic": measured_traffic(),
-                "kernel": f"conv_kernel fp32 128x128 tile with the CoC-D sums epilogue and the encode workgroups ({runs[dom].name})",
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4),
+                "traffic": measured_traffic() if args.workload == "alexnet" else None,
+                "kernel": f"conv_kernel {dtype} with the CoC-D sums epilogue and the encode workgroups "
+                          f"({runs[dom].name})",
                 "flop_per_launch": dom_flops, "avg_launch_ms": round(dom_ms, 4),
                 "all_conv_tflops": round(total_flops / (float(plain_med.sum()) * 1e-3) / 1e12, 2)}
 
     # ---- CPU oracle on a bounded sample ----------------------------------------------
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == "alexnet":
         cpu = cpu_baseline(cfg, args.cpu_seconds)
 
     value = total_flops / t_prot / 1e12
@@ -243,9 +253,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": dtype,
         "data": "synthetic",
-        "config": {"workload": "alexnet-5conv-fp32-b64", "batch": 64, "layers": nl,
+        "config": {"workload": f"{cfg.name.split('_')[0]}-{nl}conv-{'fp32' if dtype == 'f32' else 'bf16'}"
+                               f"-b{cfg.layers[0].n}",
+                   "batch": cfg.layers[0].n, "layers": nl,
                    "faults_per_step": 1, "gflop_per_step": round(total_flops / 1e9, 3)},
         "error_free_tflops": round(total_flops / t_clean / 1e12, 3),
         "unprotected_tflops": round(total_flops / t_unprot / 1e12, 3),

@@ -327,9 +327,11 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
 // rows give sum O, sum (m + wbase) O, (n + wbase) sum O and sum O^2, written as
 // slice (tile_m * N + n) of a [slices][4][E*F] float64 array; block 0 resets the
 // report.  EPI 2: EPI 1 with faults planted in the stored values first.
-// With EPI 1 and 2 the grid may also carry enc_blocks leading workgroups that
-// encode the input checksums Cd1, Cd2 of D (Sec. 3.2) instead of a tile: that
-// memory-bound work then runs beside the matrix-bound tiles of the same launch.
+// With EPI 1 and 2 the grid may also carry workgroups that encode the input
+// checksums Cd1, Cd2 of D (Sec. 3.2) instead of a tile: groups of eight
+// consecutive workgroup ids (one per XCD) are encode groups, every
+// enc_stride-th group from the start of the grid, so that the memory-bound
+// encode runs beside the matrix-bound tiles of the same launch.
 struct NoFaults {};
 constexpr int kEncVec = 4;   // columns per thread in the encode workgroups
 template <int EPI> struct Epi {
@@ -337,7 +339,9 @@ template <int EPI> struct Epi {
     ftcnn_report *rep;
     int cap;
     double *cd1, *cd2;
-    int enc_blocks;   // a multiple of 8, so tiles keep their XCD assignment
+    int enc_blocks;   // encode workgroups needed
+    int enc_groups;   // groups of eight workgroup ids given to the encode (0: none)
+    int enc_stride;   // every enc_stride-th group of eight is an encode group
     int enc_vec;      // 16-byte loads in the encode blocks
     typename std::conditional<EPI == 2, FaultList, NoFaults>::type fl;
 };
@@ -413,7 +417,7 @@ template <> struct Bits<uint16_t> {
     __device__ static float value(B b) { return bf16_bits_to_f32(b); }
 };
 
-template <typename Tr, int WM, int WP, int FM, int FP, bool WEAVE, bool KVEC, int EPI>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI>
 __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T *__restrict__ D,
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
@@ -429,12 +433,20 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     int bid = blockIdx.x;
     if constexpr (EPI != 0) {
         if (bid == 0 && tid == 0) reset_report(ep.rep, ep.cap);
-        if (bid < ep.enc_blocks) {
-            if (ep.enc_vec) encode_block<T, C::NT, kEncVec>(D, g, bid, ep.cd1, ep.cd2);
-            else encode_block<T, C::NT, 1>(D, g, bid, ep.cd1, ep.cd2);
-            return;
+        if (ep.enc_groups > 0) {
+            const int grp = bid >> 3, sub = bid & 7;
+            if (grp % ep.enc_stride == ep.enc_stride - 1 && grp / ep.enc_stride < ep.enc_groups) {
+                const int eb = (grp / ep.enc_stride) * 8 + sub;
+                if (eb < ep.enc_blocks) {
+                    if (ep.enc_vec) encode_block<T, C::NT, kEncVec>(D, g, eb, ep.cd1, ep.cd2);
+                    else encode_block<T, C::NT, 1>(D, g, eb, ep.cd1, ep.cd2);
+                }
+                return;
+            }
+            const int before = (grp + 1) / ep.enc_stride < ep.enc_groups ? (grp + 1) / ep.enc_stride : ep.enc_groups;
+            bid = (grp - before) * 8 + sub;   // keeps bid % 8, hence the XCD the tile order assumes
+            if (bid >= tiles_total) return;
         }
-        bid -= ep.enc_blocks;
     }
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wp = wave / WM;
@@ -481,7 +493,31 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     __syncthreads();
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    if constexpr (WEAVE && sizeof(T) == 4) {
+    if constexpr (WEAVE == 2 && sizeof(T) == 4) {
+        // two chunks in flight: while a chunk is consumed from one LDS buffer, the gather of the
+        // chunk two ahead is woven between its MFMAs into one register set, and the other set
+        // (the next chunk, loaded a whole chunk earlier) goes to the other buffer at the end, so
+        // no load latency is waited on.  The loop is unrolled by two so that each register set
+        // keeps its registers; chunks past the last one are fully masked (zeros, no effect).
+        Pack<T, C::VEC> ra2[C::A_PER];
+        Pack<T, C::VEC> rb2[C::KR / C::VEC];
+        uint32_t amask2 = load_a<C>(Wt, g, C::TK, KVEC, as, ra2);
+        BGather<C> bg, bg2;
+        bg2.mask = load_b<C>(D, g, C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
+        const float *A0 = reinterpret_cast<const float *>(As0), *A1 = A0 + C::TM * C::LDK;
+        const float *B0 = reinterpret_cast<const float *>(Bs0), *B1 = B0 + C::TP * C::LDK;
+        for (int kc = 0; kc < nchunks; kc += 2) {
+            chunk_f32<C, FM, FP, true>(A0, B0, lane, arow0, brow0, acc, D, Wt, g, (kc + 2) * C::TK, KVEC, as, ra,
+                                       amask, bg, bkg, pvalid, lane_base, ih0, iw0, rb);
+            store_lds<C>(As0 + C::TM * C::LDK, Bs0 + C::TP * C::LDK, tid, ra2, amask2, rb2, bg2.mask, bp, bkg);
+            __syncthreads();
+            chunk_f32<C, FM, FP, true>(A1, B1, lane, arow0, brow0, acc, D, Wt, g, (kc + 3) * C::TK, KVEC, as, ra2,
+                                       amask2, bg2, bkg, pvalid, lane_base, ih0, iw0, rb2);
+            if (kc + 2 >= nchunks) break;
+            store_lds<C>(As0, Bs0, tid, ra, amask, rb, bg.mask, bp, bkg);
+            __syncthreads();
+        }
+    } else if constexpr (WEAVE == 1 && sizeof(T) == 4) {
         // every chunk but the last: the next chunk's gather is woven between this chunk's MFMAs
         BGather<C> bg;
         for (int kc = 0; kc + 1 < nchunks; ++kc) {
@@ -647,7 +683,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     }
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP, bool WEAVE, bool KVEC, int EPI>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI>
 hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
                       const Epi<EPI> &ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
@@ -657,30 +693,40 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     const long long tiles_p = (g.P_total + C::TP - 1) / C::TP;
     const long long total = tiles_p * tiles_m;
     Epi<EPI> e = ep;
-    long long enc = 0;
+    long long grid = total;
     if constexpr (EPI != 0) {
+        e.enc_blocks = e.enc_groups = 0;
+        e.enc_stride = 1;
         if (e.cd1) {
             e.enc_vec = g.CHW % kEncVec == 0 && reinterpret_cast<uintptr_t>(D) % (kEncVec * sizeof(T)) == 0;
             const long long per = (long long)C::NT * (e.enc_vec ? kEncVec : 1);
-            enc = ((g.CHW + per - 1) / per + 7) / 8 * 8;
+            const long long eb = (g.CHW + per - 1) / per;
+            const long long eg = (eb + 7) / 8, tg = (total + 7) / 8;
+            if (eb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+            e.enc_blocks = (int)eb;
+            e.enc_groups = (int)eg;
+            // all encode groups first: they start on every CU at once and are done while the first
+            // tiles run (spreading them through the grid measured slower: late encode groups stretch
+            // the launch, interleaved ones slow the tiles beside them)
+            e.enc_stride = 1;
+            grid = 8 * (tg + eg);
         }
-        e.enc_blocks = (int)enc;
     }
-    if (total + enc > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    if (grid > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI>;
     if constexpr (C::LDS_BYTES > 65536) {
         static const hipError_t attr = hipFuncSetAttribute(
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
         if (attr != hipSuccess) return attr;
     }
-    kern<<<(unsigned)(total + enc), C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D),
+    kern<<<(unsigned)grid, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D),
                                                                static_cast<const T *>(W), static_cast<T *>(O), g,
                                                                tiles_m, (int)total, m_major, e);
     return hipGetLastError();
 }
 
 // One tile configuration, dispatched on the weight alignment and the epilogue.
-template <typename Tr, int WM, int WP, int FM, int FP, bool WEAVE> struct Tile {
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     static constexpr int TM = WM * FM * 32;
     template <int EPI>
     static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep) {
@@ -743,10 +789,10 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
                             hipStream_t st) {
     double *part = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_sums);
     if (nf == 0) {
-        Epi<1> ep{part, rep, cap, cd1, cd2, 0, 0, {}};
+        Epi<1> ep{part, rep, cap, cd1, cd2, 0, 0, 1, 0, {}};
         return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
     }
-    Epi<2> ep{part, rep, cap, cd1, cd2, 0, 0, {}};
+    Epi<2> ep{part, rep, cap, cd1, cd2, 0, 0, 1, 0, {}};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
     return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });

@@ -635,15 +635,43 @@ __device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double 
     int r = rem / g.S, s = rem - r * g.S;
     const int dch = TPP / RS, drem = TPP - dch * RS, dr = drem / g.S, ds = drem - dr * g.S;
     const int ih0 = g.U * x - g.P, iw0 = g.U * y - g.P;
-    for (int k = lane; k < g.K; k += TPP) {
+    // branch-free taps, four in flight: a tap in the zero padding reads element 0 and selects 0
+    constexpr int U4 = 4;
+    int k = lane;
+    for (; k + (U4 - 1) * TPP < g.K; k += U4 * TPP) {
+        double d1[U4], d2[U4], w1[U4], w2[U4], ok[U4];
+#pragma unroll
+        for (int u = 0; u < U4; ++u) {
+            const int ih = ih0 + r, iw = iw0 + s;
+            const bool in = ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
+            const long long off = in ? ((long long)ch * g.H + ih) * g.W + iw : 0;
+            d1[u] = c.cd1[off];
+            d2[u] = c.cd2[off];
+            w1[u] = c.cw1[k + u * TPP];
+            w2[u] = c.cw2[k + u * TPP];
+            ok[u] = in ? 1.0 : 0.0;
+            s += ds;
+            r += dr;
+            ch += dch;
+            if (s >= g.S) { s -= g.S; ++r; }
+            if (r >= g.R) { r -= g.R; ++ch; }
+        }
+#pragma unroll
+        for (int u = 0; u < U4; ++u) {
+            const double a1 = ok[u] != 0.0 ? d1[u] : 0.0, a2 = ok[u] != 0.0 ? d2[u] : 0.0;
+            c5 = fma(a1, w1[u], c5);
+            c6 = fma(a1, w2[u], c6);
+            c7 = fma(a2, w1[u], c7);
+        }
+    }
+    for (; k < g.K; k += TPP) {
         const int ih = ih0 + r, iw = iw0 + s;
         if ((unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W) {
             const long long off = ((long long)ch * g.H + ih) * g.W + iw;
             const double d1 = c.cd1[off], d2 = c.cd2[off];
-            const double w1 = c.cw1[k], w2 = c.cw2[k];
-            c5 = fma(d1, w1, c5);
-            c6 = fma(d1, w2, c6);
-            c7 = fma(d2, w1, c7);
+            c5 = fma(d1, c.cw1[k], c5);
+            c6 = fma(d1, c.cw2[k], c6);
+            c7 = fma(d2, c.cw1[k], c7);
         }
         s += ds;
         r += dr;
@@ -798,7 +826,7 @@ hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, cons
     const double *part = reinterpret_cast<const double *>(w + off_part);
     int *flags = reinterpret_cast<int *>(w + pl.off_flags);
     double *scratch = reinterpret_cast<double *>(w + pl.off_corr);
-    const int tpp = final_tpp(sp, coc ? pl.g.K : 0);
+    const int tpp = final_tpp(sp, coc ? pl.g.K : 0, pl.g.EF);
     const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
 #define VC(TPP, COC)                                                                                       \
     verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, ck.co5, ck.co6, ck.co7,   \

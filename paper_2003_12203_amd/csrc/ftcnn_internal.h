@@ -140,12 +140,18 @@ hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void 
                                       const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
                                       bool coc, void *ws, hipStream_t st);
 
-// Threads that share one position in the final verification stage (a power of
-// two; the float64 split partials of that position, and the K taps of its
-// Co5..Co7 when those are computed there too, are spread over them).
-inline int final_tpp(int splits, int taps = 0) {
-    const int w = splits > taps / 4 ? splits : taps / 4;
-    return w <= 1 ? 1 : w <= 4 ? 4 : w <= 16 ? 16 : w <= 128 ? 64 : kThreads;
+// Threads that share one position in the final verification stage (1, 4, 16,
+// 64 or a whole workgroup; the float64 split partials of that position, and the
+// K taps of its Co5..Co7 when those are computed there too, are spread over
+// them): enough lanes for the work of one position, but no more than keeps the
+// whole grid to about two million threads.
+inline int final_tpp(int splits, int taps, long long positions) {
+    const long long w = (long long)splits + taps;
+    int t = 1;
+    while (t < kThreads && 2LL * t < w) t *= 4;
+    if (t > kThreads) t = kThreads;
+    while (t > 1 && (long long)t * positions > (2LL << 20)) t /= 4;
+    return t;
 }
 hipError_t launch_inject(const Plan &pl, void *O, const ftcnn_fault *f, int nf, hipStream_t st);
 
