@@ -136,7 +136,7 @@ def main():
         for li, r in enumerate(runs):
             if ev is not None:
                 ev[li][0].record()
-            r.lay.conv(r.D, r.W, r.O)
+            r.lay.conv_ws(r.D, r.W, r.O)
             if ev is not None:
                 ev[li][1].record()
 

@@ -206,16 +206,27 @@ int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void 
                          const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                          int32_t cap_fixes, void *workspace, hipStream_t stream);
 
-/* Eq. (1) as ftcnn_conv_fwd (same main loop, bitwise the same O), with the
+/* Eq. (1) as ftcnn_conv_fwd, through the path the protected calls below use:
+ * for layers with ch a multiple of 32, D and W are first copied channels-last
+ * into the workspace (D as [n][h][w][ch], W as [m][r][s][ch]) so that the
+ * convolution gathers 16-byte runs; K is then summed in (r, s, ch) order, so
+ * O may differ from ftcnn_conv_fwd's in the last bits (both are eq. (1) with
+ * fp32 accumulation).  O is bitwise that of ftcnn_conv_fwd_sums.  Other layers
+ * take ftcnn_conv_fwd's kernel.  Needs the workspace of ftcnn_workspace_bytes. */
+int ftcnn_conv_fwd_ws(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                      void *workspace, hipStream_t stream);
+
+/* Eq. (1) as ftcnn_conv_fwd_ws (same kernels, bitwise the same O), with the
  * CoC-D summations of Sec. 3.6 computed in the epilogue from the values as
  * stored: every workgroup tile writes, for each of its output pixels, the
  * partial So5, So6, So7 and sum of squares over its filters into the
  * workspace, so detection never re-reads O.  Also resets *rep (cap_fixes
  * recorded).  Follow it with ftcnn_verify_correct_sums on the same workspace
  * and report.
- * ck: may be NULL.  When ck->cd1 and ck->cd2 are set, additional workgroups of
- * the same launch encode them from D as ftcnn_encode(which = 0) does (Sec.
- * 3.2), beside the matrix-core tiles; other members are not used.
+ * ck: may be NULL.  When ck->cd1 and ck->cd2 are set, additional workgroups
+ * encode them from D as ftcnn_encode(which = 0) does (Sec. 3.2), in the
+ * launch that makes the channels-last copies or beside the matrix-core tiles;
+ * other members are not used.
  * faults / nf: TEST ONLY, NULL / 0 otherwise.  A HOST array of at most 64
  * faults planted in the output values before they are summed and stored, as
  * a fault of the convolution's own arithmetic would appear (Sec. 6.1).
@@ -236,9 +247,9 @@ int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const 
                               const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                               uint32_t which, void *workspace, hipStream_t stream);
 
-/* The whole path of one protected layer on one stream, in two launches:
+/* The whole path of one protected layer on one stream:
  * conv_fwd_sums (with the encode of Cd1, Cd2) -> verify_correct_sums (with
- * Co5..Co7).  ck->cw1/cw2 must hold the encoded W (ftcnn_encode with
+ * Co5..Co7): two launches, three for channels-last layers.  ck->cw1/cw2 must hold the encoded W (ftcnn_encode with
  * which = 1); ck->cd1, cd2, co5..co7, so5..so7 and q5 are written. */
 int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                          const ftcnn_checksums *ck, const ftcnn_policy *policy,

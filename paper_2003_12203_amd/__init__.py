@@ -113,6 +113,11 @@ def verify_correct(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
            "ftcnn_verify_correct")
 
 
+def conv_fwd_ws(desc, D, W, O, workspace, stream=None) -> None:
+    _check(lib().ftcnn_conv_fwd_ws(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), _ptr(workspace), _stream(stream)),
+           "ftcnn_conv_fwd_ws")
+
+
 def conv_fwd_sums(desc, D, W, O, ck, report, cap, workspace, faults: Sequence[dict] = (), stream=None) -> None:
     arr = _fault_array(faults)
     _check(lib().ftcnn_conv_fwd_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck) if ck else None,
@@ -247,6 +252,10 @@ class Layer:
 
     def verify_correct(self, D, W, O, stream=None):
         verify_correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace, stream)
+
+    def conv_ws(self, D, W, O, stream=None):
+        """ftcnn_conv_fwd_ws: the convolution through the protected path's kernels."""
+        conv_fwd_ws(self.desc, D, W, O, self.workspace, stream)
 
     def conv_sums(self, D, W, O, faults=(), stream=None, encode=False):
         """ftcnn_conv_fwd_sums; encode=True also encodes Cd1, Cd2 of D in the same launch."""

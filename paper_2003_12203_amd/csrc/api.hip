@@ -101,6 +101,13 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     off += align256(4ull * pl->ver_splits * EF * sizeof(double));
     pl->off_sums = off;
     off += align256(4ull * pl->sum_splits * EF * sizeof(double));
+    // channels-last copies of D and W for the vector-gather convolution
+    pl->nhwc = nhwc_layer(g);
+    const size_t es = g.dtype == FTCNN_F32 ? 4 : 2;
+    pl->off_dt = off;
+    off += pl->nhwc ? align256((size_t)g.N * CHW * es) : 0;
+    pl->off_wt = off;
+    off += pl->nhwc ? align256((size_t)g.M * K * es) : 0;
     pl->off_corr = off;
     off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
     pl->bytes = off;
@@ -326,6 +333,16 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
     FT_TRY(do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, nullptr, 0, workspace, stream));
     return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, workspace,
                                   stream);
+}
+
+int ftcnn_conv_fwd_ws(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O, void *workspace,
+                      hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (!D || !W || !O) return fail(FTCNN_E_ARG, "conv_fwd_ws: null pointer");
+    FT_TRY(check_ws(pl, workspace));
+    FT_HIP(launch_conv_ws(pl, D, W, O, workspace, stream), "conv_fwd_ws");
+    return FTCNN_OK;
 }
 
 int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,

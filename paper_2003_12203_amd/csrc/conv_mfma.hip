@@ -17,6 +17,7 @@
 #include <type_traits>
 
 #include "ftcnn_internal.h"
+#include "encode_block.h"
 
 namespace ftcnn {
 namespace {
@@ -242,6 +243,39 @@ __device__ inline void mma_bf16(const uint16_t *As, const uint16_t *Bs, int lane
     }
 }
 
+// One chunk of MFMAs from LDS for either element type.
+template <typename C, int FM, int FP>
+__device__ inline void mma_chunk(const typename C::T *As, const typename C::T *Bs, int lane, int arow0, int brow0,
+                                 floatx16 (&acc)[FM][FP]) {
+    if constexpr (sizeof(typename C::T) == 4)
+        mma_f32<C::TK, FM, FP>(reinterpret_cast<const float *>(As), reinterpret_cast<const float *>(Bs), lane, arow0,
+                               brow0, acc);
+    else
+        mma_bf16<C::TK, FM, FP>(reinterpret_cast<const uint16_t *>(As), reinterpret_cast<const uint16_t *>(Bs), lane,
+                                arow0, brow0, acc);
+}
+
+// The B gather from channels-last Dt[n][h][w][c] with K in (r, s, c) order: a
+// thread's run of KR consecutive k lies inside one (r, s) (Ch is a multiple of
+// the chunk), so it is KR contiguous elements of one input pixel, loaded as
+// 16-byte units; the padding test is one test for the whole run.
+template <typename C>
+__device__ inline uint32_t load_b_nhwc(const typename C::T *__restrict__ Dt, const Geom &g, int kstart_lane,
+                                       bool pvalid, int img_base, int ih0, int iw0,
+                                       Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+    const int kstart = __builtin_amdgcn_readfirstlane(kstart_lane);
+    const int rs = kstart / g.C, c0 = kstart - rs * g.C;
+    const int r = rs / g.S, s = rs - r * g.S;
+    const int ih = ih0 + r, iw = iw0 + s;
+    const bool ok = pvalid & (kstart < g.K) & ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
+    const int base = ok ? img_base + (ih * g.W + iw) * g.C + c0 : 0;   // a multiple of KR: 16-byte aligned
+    const uint4 *src = reinterpret_cast<const uint4 *>(Dt + base);
+#pragma unroll
+    for (int i = 0; i < C::KR / C::VEC; ++i) rb[i].q = src[i];
+    constexpr uint32_t all = C::KR == 32 ? 0xFFFFFFFFu : ((1u << C::KR) - 1u);
+    return ok ? all : 0u;
+}
+
 // Stateful form of the B gather, so that its elements can be issued one at a
 // time between MFMAs: (c, r, s) and the k offset advance in scalar registers.
 template <typename C> struct BGather {
@@ -333,7 +367,6 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
 // enc_stride-th group from the start of the grid, so that the memory-bound
 // encode runs beside the matrix-bound tiles of the same launch.
 struct NoFaults {};
-constexpr int kEncVec = 4;   // columns per thread in the encode workgroups
 template <int EPI> struct Epi {
     double *part;
     ftcnn_report *rep;
@@ -347,64 +380,6 @@ template <int EPI> struct Epi {
 };
 template <> struct Epi<0> {};
 
-// V elements of one row of D, loaded as one unit (V * sizeof(T) is 2 to 16 bytes).
-template <typename T, int V> union RowPack {
-    using Q = typename std::conditional<
-        V * sizeof(T) == 16, uint4,
-        typename std::conditional<V * sizeof(T) == 8, uint2,
-                                  typename std::conditional<V * sizeof(T) == 4, uint32_t, uint16_t>::type>::type>::type;
-    Q q;
-    T e[V];
-};
-
-// One encode workgroup: V consecutive columns of D viewed as [N][Ch*H*W] per
-// thread, every row n in order (eight rows of loads in flight), accumulated in
-// float64: Cd1 = sum_n D_n and Cd2 = sum_n (n + wbase) D_n.
-template <typename T, int NT, int V>
-__device__ void encode_block(const T *__restrict__ D, const Geom &g, int blk, double *__restrict__ cd1,
-                             double *__restrict__ cd2) {
-    const long long col = ((long long)blk * NT + threadIdx.x) * V;
-    if (col >= g.CHW) return;
-    const int nv = (long long)V <= g.CHW - col ? V : (int)(g.CHW - col);   // V == 1 whenever Ch*H*W % V != 0
-    double a1[V], a2[V];
-#pragma unroll
-    for (int e = 0; e < V; ++e) a1[e] = a2[e] = 0.0;
-    const T *src = D + col;
-    // rows stay packed in registers until they are added (V elements per row in flight)
-    using P = RowPack<T, V>;
-    auto load = [&](long long row) -> P {
-        P pk;
-        pk.q = *reinterpret_cast<const typename P::Q *>(src + row * g.CHW);
-        return pk;
-    };
-    auto add = [&](const P &pk, int n) {
-        const double w = (double)(n + g.wbase);
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-            double x;
-            if constexpr (sizeof(T) == 4) x = (double)pk.e[e];
-            else x = (double)bf16_bits_to_f32(pk.e[e]);
-            a1[e] += x;
-            a2[e] = fma(w, x, a2[e]);
-        }
-    };
-    int n = 0;
-    for (; n + 7 < g.N; n += 8) {
-        P v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = load(n + u);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) add(v[u], n + u);
-    }
-    for (; n < g.N; ++n) add(load(n), n);
-#pragma unroll
-    for (int e = 0; e < V; ++e)
-        if (e < nv) {
-            cd1[col + e] = a1[e];
-            cd2[col + e] = a2[e];
-        }
-}
-
 template <typename T> struct Bits;
 template <> struct Bits<float> {
     using B = float;   // an fp32 output is stored as computed
@@ -417,7 +392,7 @@ template <> struct Bits<uint16_t> {
     __device__ static float value(B b) { return bf16_bits_to_f32(b); }
 };
 
-template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC>
 __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T *__restrict__ D,
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
@@ -471,7 +446,8 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         const int x = pix / g.F, y = pix - (pix / g.F) * g.F;
         ih0 = g.U * x - g.P;
         iw0 = g.U * y - g.P;
-        lane_base = n * (int)g.CHW + ih0 * g.W + iw0;
+        // channels-last: the image's base in Dt; otherwise the pixel's first tap in D
+        lane_base = NHWC ? n * (int)g.CHW : n * (int)g.CHW + ih0 * g.W + iw0;
     }
     ASlots<C> as;
     a_slots<C>(g, m0, tid, as);
@@ -488,12 +464,28 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
     uint32_t amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
-    uint32_t bmask = load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+    uint32_t bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
+                          : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
     store_lds<C>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
     __syncthreads();
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    if constexpr (WEAVE == 2 && sizeof(T) == 4) {
+    if constexpr (NHWC) {
+        // channels-last: a whole chunk's gather is a few 16-byte loads per thread, issued
+        // before this chunk's MFMAs and stored after them
+        for (int kc = 0; kc + 1 < nchunks; ++kc) {
+            const int buf = kc & 1;
+            const int kb = (kc + 1) * C::TK;
+            amask = load_a<C>(Wt, g, kb, KVEC, as, ra);
+            bmask = load_b_nhwc<C>(D, g, kb + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+            mma_chunk<C, FM, FP>(As0 + buf * C::TM * C::LDK, Bs0 + buf * C::TP * C::LDK, lane, arow0, brow0, acc);
+            store_lds<C>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
+                         bmask, bp, bkg);
+            __syncthreads();
+        }
+        mma_chunk<C, FM, FP>(As0 + ((nchunks - 1) & 1) * C::TM * C::LDK, Bs0 + ((nchunks - 1) & 1) * C::TP * C::LDK,
+                             lane, arow0, brow0, acc);
+    } else if constexpr (WEAVE == 2 && sizeof(T) == 4) {
         // two chunks in flight: while a chunk is consumed from one LDS buffer, the gather of the
         // chunk two ahead is woven between its MFMAs into one register set, and the other set
         // (the next chunk, loaded a whole chunk earlier) goes to the other buffer at the end, so
@@ -683,7 +675,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     }
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC>
 hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
                       const Epi<EPI> &ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
@@ -713,7 +705,7 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
         }
     }
     if (grid > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI>;
+    auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI, NHWC>;
     if constexpr (C::LDS_BYTES > 65536) {
         static const hipError_t attr = hipFuncSetAttribute(
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
@@ -728,11 +720,14 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
 // One tile configuration, dispatched on the weight alignment and the epilogue.
 template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     static constexpr int TM = WM * FM * 32;
+    // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
     template <int EPI>
-    static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep) {
+    static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep,
+                          bool nhwc = false) {
+        if (nhwc) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, ep);
         const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
-        if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI>(g, D, W, O, st, 0, ep);
-        return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI>(g, D, W, O, st, 0, ep);
+        if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, false>(g, D, W, O, st, 0, ep);
+        return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI, false>(g, D, W, O, st, 0, ep);
     }
 };
 
@@ -787,15 +782,34 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
 hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, double *cd1, double *cd2,
                             ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
                             hipStream_t st) {
-    double *part = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_sums);
+    char *w = static_cast<char *>(ws);
+    double *part = reinterpret_cast<double *>(w + pl.off_sums);
+    const void *Dc = D, *Wc = W;
+    if (pl.nhwc) {
+        // channels-last copies; the encode (if asked) rides in the same launch
+        const hipError_t e = launch_prep(pl, D, W, cd1, cd2, ws, st);
+        if (e != hipSuccess) return e;
+        Dc = w + pl.off_dt;
+        Wc = w + pl.off_wt;
+        cd1 = cd2 = nullptr;
+    }
     if (nf == 0) {
         Epi<1> ep{part, rep, cap, cd1, cd2, 0, 0, 1, 0, {}};
-        return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
+        return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc); });
     }
     Epi<2> ep{part, rep, cap, cd1, cd2, 0, 0, 1, 0, {}};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
-    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
+    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc); });
+}
+
+hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st) {
+    if (!pl.nhwc) return launch_conv(pl, D, W, O, st);
+    const hipError_t e = launch_prep(pl, D, W, nullptr, nullptr, ws, st);
+    if (e != hipSuccess) return e;
+    char *w = static_cast<char *>(ws);
+    const Epi<0> ep{};
+    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, w + pl.off_dt, w + pl.off_wt, O, st, ep, true); });
 }
 
 }  // namespace ftcnn

@@ -32,7 +32,8 @@ struct Plan {
     int corr_blocks;                  // workgroups of the correction kernel
     int corr_slots;                   // per-workgroup scratch slices (correction or fused verification)
     int sum_splits;                   // partial-sum slices written by the convolution epilogue
-    size_t off_flags, off_enc, off_ver, off_sums, off_corr, bytes;
+    bool nhwc;                        // the convolution reads channels-last copies of D and W
+    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
 
@@ -121,6 +122,15 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
                             hipStream_t st);
 // Rows of C per workgroup tile of the convolution chosen for this layer.
 int conv_tile_m(const Geom &g);
+// Layers whose convolution reads channels-last copies (pl.nhwc): Ch a multiple of 32.
+inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0; }
+// Dt = D in [n][h][w][c] order and Wt = W in [m][r][s][c] order into the workspace
+// (pl.off_dt, pl.off_wt); with cd1 and cd2 set, the same launch encodes them.
+hipError_t launch_prep(const Plan &pl, const void *D, const void *W, double *cd1, double *cd2, void *ws,
+                       hipStream_t st);
+// The convolution alone through the path ftcnn_conv_fwd_sums takes (channels-last
+// copies for pl.nhwc layers): O bitwise equal to that of launch_conv_sums.
+hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st);
 hipError_t launch_checksum_conv(const Plan &pl, uint32_t which, const void *D, const void *W,
                                 const ftcnn_checksums &ck, hipStream_t st);
 hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &ck,

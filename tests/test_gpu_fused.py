@@ -1,7 +1,7 @@
 """The convolution with the CoC-D summations in its epilogue (ftcnn_conv_fwd_sums) against the
 separate kernels and the oracle.
 
-* O is bitwise the output of ftcnn_conv_fwd (same main loop, same rounding);
+* O is bitwise the output of ftcnn_conv_fwd_ws (same kernels, same rounding);
 * So5, So6, So7 and Q5 from the epilogue partials agree with the oracle's summations of the
   GPU's own output (Sec. 3.6) to float64 rounding, and exactly on integer data;
 * faults planted in the epilogue give bitwise the output that ftcnn_inject gives afterwards;
@@ -36,14 +36,14 @@ def test_epilogue_sums_match_oracle(cfg, li, spec, wbase):
     lay.encode_weights(Wd)
     lay.encode_input(Dd)
     O_ref = lay.empty_output()
-    lay.conv(Dd, Wd, O_ref)
+    lay.conv_ws(Dd, Wd, O_ref)
     O = lay.empty_output()
     lay.conv_sums(Dd, Wd, O)
     lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
     lay.verify_correct_sums(Dd, Wd, O)
     torch.cuda.synchronize()
     assert torch.equal(O.view(torch.int16 if spec.dtype == "bf16" else torch.int32),
-                       O_ref.view(torch.int16 if spec.dtype == "bf16" else torch.int32)), "O differs from conv_fwd"
+                       O_ref.view(torch.int16 if spec.dtype == "bf16" else torch.int32)), "O differs from conv_fwd_ws"
     got = _sums(lay)
     co5 = lay.buf["co5"].cpu().numpy().reshape(lay.E, lay.F)
     so5, so6, so7, q5, flags = wf.verify(host(O), co5, spec.ch * spec.r * spec.s, spec.dtype,
@@ -63,13 +63,13 @@ def test_two_launch_checksums_match_oracle(cfg, li, spec):
     Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
     lay.encode_weights(Wd)
     O_ref = lay.empty_output()
-    lay.conv(Dd, Wd, O_ref)
+    lay.conv_ws(Dd, Wd, O_ref)
     O = lay.empty_output()
     lay.conv_sums(Dd, Wd, O, encode=True)
     lay.verify_correct_sums(Dd, Wd, O, coc=True)
     torch.cuda.synchronize()
     iv = torch.int16 if spec.dtype == "bf16" else torch.int32
-    assert torch.equal(O.view(iv), O_ref.view(iv)), "O differs from conv_fwd"
+    assert torch.equal(O.view(iv), O_ref.view(iv)), "O differs from conv_fwd_ws"
     b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
     cd1, cd2 = wf.encode(D, 0)
     np.testing.assert_allclose(b["cd1"], cd1.ravel(), rtol=1e-12, atol=1e-12)
@@ -159,7 +159,7 @@ def test_planted_faults_equal_injected(dtype):
     lay.encode_weights(Wd)
     lay.encode_input(Dd)
     O1 = lay.empty_output()
-    lay.conv(Dd, Wd, O1)
+    lay.conv_ws(Dd, Wd, O1)
     lay.inject(O1, to_ft_faults(faults))
     O2 = lay.empty_output()
     lay.conv_sums(Dd, Wd, O2, to_ft_faults(faults))
@@ -207,7 +207,7 @@ def test_protected_conv_single_call(li):
     assert not rep.detected and rep.status == ft.STATUS_CLEAN
     O2 = lay.empty_output()
     lay.encode_input(Dd)
-    lay.conv(Dd, Wd, O2)
+    lay.conv_ws(Dd, Wd, O2)
     lay.checksum_conv(ft.CO5 | ft.CO6 | ft.CO7)
     lay.verify(O2)
     torch.cuda.synchronize()
