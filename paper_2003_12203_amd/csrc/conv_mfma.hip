@@ -731,11 +731,12 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     }
 };
 
-// Tile choice per layer (fp32 rules from a sweep over the workload shapes on
-// MI355X): the filter tile follows M so small-M layers waste no MFMA rows; for
-// larger M the biggest tile that still leaves about two workgroups per CU wins,
-// except that layers with large W (M >= 512, K >= 4096) prefer 256-row tiles,
-// which halve the im2col traffic per flop.
+// Tile choice per layer, from sweeps over the workload shapes on MI355X.  The
+// filter tile follows M so small-M layers waste no MFMA rows; for larger M the
+// biggest tile that still leaves about two workgroups per CU wins.  For bf16
+// (eight times the fp32 matrix rate per instruction) layers with many pixel
+// tiles take 256-row filter tiles, and the others a 64 x 128 tile with
+// 64-deep chunks (fewer barriers per flop; needs Ch % 64 == 0 channels-last).
 long long n_tiles(const Geom &g, int tm, int tp) {
     return ((g.P_total + tp - 1) / tp) * (long long)((g.M + tm - 1) / tm);
 }
@@ -743,28 +744,31 @@ long long n_tiles(const Geom &g, int tm, int tp) {
 using F32_M32 = Tile<F32T<16>, 1, 4, 1, 2, true>;
 using F32_M64 = Tile<F32T<16>, 2, 2, 1, 2, true>;
 using F32_M96 = Tile<F32T<16>, 1, 4, 3, 2, true>;
-using F32_256x128 = Tile<F32T<16>, 4, 2, 2, 2, true>;
 using F32_128x128 = Tile<F32T<16>, 2, 2, 2, 2, true>;
 using F32_128x64 = Tile<F32T<32>, 2, 2, 2, 1, true>;
 using F32_64x64 = Tile<F32T<32>, 2, 2, 1, 1, true>;
 using BF16_M32 = Tile<BF16T<32>, 1, 4, 1, 2, false>;
 using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, false>;
 using BF16_128x128 = Tile<BF16T<32>, 2, 2, 2, 2, false>;
+using BF16_256x128 = Tile<BF16T<32>, 4, 2, 2, 2, false>;
+using BF16_64x128_K64 = Tile<BF16T<64>, 2, 2, 1, 2, false>;
 
-// Calls f.template operator()<TileType>() for the tile this layer uses.
+// Calls f(TileType{}) for the tile this layer uses.
 template <typename Fn>
 auto with_tile(const Geom &g, Fn &&f) {
     if (g.dtype == FTCNN_F32) {
         if (g.M <= 32) return f(F32_M32{});
         if (g.M <= 64) return f(F32_M64{});
         if (g.M <= 96) return f(F32_M96{});
-        if (g.M >= 512 && g.K >= 4096 && n_tiles(g, 256, 128) >= 256) return f(F32_256x128{});
         if (n_tiles(g, 128, 128) >= 600) return f(F32_128x128{});
         if (n_tiles(g, 128, 64) >= 380) return f(F32_128x64{});
         return f(F32_64x64{});
     }
     if (g.M <= 32) return f(BF16_M32{});
     if (g.M <= 64) return f(BF16_M64{});
+    if (g.M <= 128) return f(BF16_128x128{});
+    if (n_tiles(g, 256, 128) >= 192) return f(BF16_256x128{});
+    if (g.C % 64 == 0) return f(BF16_64x128_K64{});
     return f(BF16_128x128{});
 }
 
