@@ -223,10 +223,14 @@ int ftcnn_conv_fwd_ws(const ftcnn_conv_desc *desc, const void *D, const void *W,
  * workspace, so detection never re-reads O.  Also resets *rep (cap_fixes
  * recorded).  Follow it with ftcnn_verify_correct_sums on the same workspace
  * and report.
- * ck: may be NULL.  When ck->cd1 and ck->cd2 are set, additional workgroups
- * encode them from D as ftcnn_encode(which = 0) does (Sec. 3.2), in the
- * launch that makes the channels-last copies or beside the matrix-core tiles;
- * other members are not used.
+ * ck: may be NULL.  When ck->cd1 and ck->cd2 are set, Cd1 and Cd2 are encoded
+ * from D as ftcnn_encode(which = 0) does (Sec. 3.2): by the channels-last copy
+ * of D as it moves the values, or by extra workgroups beside the matrix-core
+ * tiles.  When ck->cw1 and ck->cw2 (the encoded W) are set as well, layers
+ * with ch a multiple of 32 also compute the products Co5, Co6, Co7 of Sec. 3.2
+ * in extra workgroups of the convolution launch, as per-channel-range partials
+ * in the workspace that ftcnn_verify_correct_sums(which = CO5|CO6|CO7) adds up.
+ * Other members are not used.
  * faults / nf: TEST ONLY, NULL / 0 otherwise.  A HOST array of at most 64
  * faults planted in the output values before they are summed and stored, as
  * a fault of the convolution's own arithmetic would appear (Sec. 6.1).
@@ -239,17 +243,19 @@ int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *
  * the workspace (one launch; O is read only at flagged positions).  The
  * report must be the one ftcnn_conv_fwd_sums reset.  which = 0: Co5..Co7 are
  * read from ck (ftcnn_checksum_conv ran before); which = FTCNN_CO5 |
- * FTCNN_CO6 | FTCNN_CO7: the same launch computes them from ck->cd1, cd2,
- * cw1, cw2 at every position first and stores them in ck->co5, co6, co7.
- * Writes ck->so5, so6, so7, q5 and the flag map; same decisions and repairs
- * as ftcnn_verify_correct. */
+ * FTCNN_CO6 | FTCNN_CO7: the same launch produces them at every position
+ * first, adding the partial products ftcnn_conv_fwd_sums computed (when it
+ * did) or else evaluating them from ck->cd1, cd2, cw1, cw2, and stores them in
+ * ck->co5, co6, co7.  Writes ck->so5, so6, so7, q5 and the flag map; same
+ * decisions and repairs as ftcnn_verify_correct. */
 int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                               const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                               uint32_t which, void *workspace, hipStream_t stream);
 
 /* The whole path of one protected layer on one stream:
- * conv_fwd_sums (with the encode of Cd1, Cd2) -> verify_correct_sums (with
- * Co5..Co7): two launches, three for channels-last layers.  ck->cw1/cw2 must hold the encoded W (ftcnn_encode with
+ * conv_fwd_sums (with the encode of Cd1, Cd2, and Co5..Co7 on channels-last
+ * layers) -> verify_correct_sums (with Co5..Co7): two launches, three for
+ * channels-last layers.  ck->cw1/cw2 must hold the encoded W (ftcnn_encode with
  * which = 1); ck->cd1, cd2, co5..co7, so5..so7 and q5 are written. */
 int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                          const ftcnn_checksums *ck, const ftcnn_policy *policy,

@@ -258,11 +258,13 @@ class Layer:
         conv_fwd_ws(self.desc, D, W, O, self.workspace, stream)
 
     def conv_sums(self, D, W, O, faults=(), stream=None, encode=False):
-        """ftcnn_conv_fwd_sums; encode=True also encodes Cd1, Cd2 of D in the same launch."""
+        """ftcnn_conv_fwd_sums; encode=True also encodes Cd1, Cd2 of D in the same pass and, on
+        channels-last layers, computes the Co5..Co7 partials from them and Cw1, Cw2."""
         ck = None
         if encode:
             ck = _lib.Checksums()
             ck.cd1, ck.cd2 = self.buf["cd1"].data_ptr(), self.buf["cd2"].data_ptr()
+            ck.cw1, ck.cw2 = self.buf["cw1"].data_ptr(), self.buf["cw2"].data_ptr()
         conv_fwd_sums(self.desc, D, W, O, ck, self.report, self.cap, self.workspace, faults, stream)
 
     def verify_correct_sums(self, D, W, O, stream=None, coc=False):

@@ -101,13 +101,47 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     off += align256(4ull * pl->ver_splits * EF * sizeof(double));
     pl->off_sums = off;
     off += align256(4ull * pl->sum_splits * EF * sizeof(double));
-    // channels-last copies of D and W for the vector-gather convolution
+    // channels-last copies of D and W for the vector-gather convolution; the copy of D encodes
+    // Cd1, Cd2 too, over image ranges when the layer has few 32 x 32 tiles.  A range keeps at least
+    // 64 bytes of D per element of its float64 partial pair (16 images in fp32, 32 in bf16), so the
+    // partials cost at most a quarter of D's traffic
     pl->nhwc = nhwc_layer(g);
     const size_t es = g.dtype == FTCNN_F32 ? 4 : 2;
+    pl->prep_ns = 1;
+    pl->co_in_conv = false;
+    pl->co = CocTile{1, 1, 1, 1, 1, 1, 0, 1};
+    if (pl->nhwc) {
+        const long long tiles = (long long)(g.C / 32) * ceil_div((long long)g.H * g.W, 32);
+        const int min_imgs = g.dtype == FTCNN_F32 ? 16 : 32;
+        pl->prep_ns = clampi(ceil_div(1024, tiles), 1, g.N / min_imgs > 1 ? g.N / min_imgs : 1);
+        // Co5..Co7 in extra workgroups of the convolution launch, in its threads and LDS
+        int nt = 0;
+        size_t lds = 0;
+        conv_tile_shape(g, &nt, &lds);
+        CocTile &co = pl->co;
+        co.tx = g.F >= 24 ? 32 : (g.F >= 12 ? 16 : 8);
+        co.ty = nt / co.tx < g.E ? nt / co.tx : g.E;
+        auto window = [&](int ty) { return (size_t)((ty - 1) * g.U + g.R) * ((co.tx - 1) * g.U + g.S); };
+        while (co.ty > 1 && 2 * sizeof(double) * window(co.ty) > lds) co.ty /= 2;
+        if (2 * sizeof(double) * window(co.ty) <= lds) {
+            pl->co_in_conv = true;
+            const size_t cc = lds / (2 * sizeof(double) * window(co.ty));
+            co.cc = (int)(cc < 8 ? cc : 8);
+            co.tiles_x = (int)ceil_div(g.F, co.tx);
+            co.tiles = (int)(ceil_div(g.E, co.ty) * co.tiles_x);
+            co.groups = clampi(ceil_div(768, co.tiles), 1, ceil_div(g.C, co.cc));
+        }
+        co.ns = pl->prep_ns;
+        co.comb_blocks = pl->prep_ns > 1 ? (int)ceil_div(CHW, 2LL * nt) : 0;
+    }
     pl->off_dt = off;
     off += pl->nhwc ? align256((size_t)g.N * CHW * es) : 0;
     pl->off_wt = off;
     off += pl->nhwc ? align256((size_t)g.M * K * es) : 0;
+    pl->off_encp = off;
+    off += pl->prep_ns > 1 ? align256(2ull * pl->prep_ns * CHW * sizeof(double)) : 0;
+    pl->off_copart = off;
+    off += pl->co_in_conv ? align256(3ull * pl->co.groups * EF * sizeof(double)) : 0;
     pl->off_corr = off;
     off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
     pl->bytes = off;
@@ -223,11 +257,13 @@ int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ft
                  ftcnn_report *rep, int32_t cap, const ftcnn_fault *faults, int32_t nf, void *ws, hipStream_t st) {
     if (!D || !W || !O || !rep) return fail(FTCNN_E_ARG, "conv_fwd_sums: null pointer");
     if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
-    double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
+    const double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
     if ((cd1 == nullptr) != (cd2 == nullptr)) return fail(FTCNN_E_ARG, "conv_fwd_sums: cd1 and cd2 go together");
+    if (ck && ((ck->cw1 == nullptr) != (ck->cw2 == nullptr)))
+        return fail(FTCNN_E_ARG, "conv_fwd_sums: cw1 and cw2 go together");
     FT_TRY(check_faults(pl.g, faults, nf, "conv_fwd_sums"));
     FT_TRY(check_ws(pl, ws));
-    FT_HIP(launch_conv_sums(pl, D, W, O, cd1, cd2, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
+    FT_HIP(launch_conv_sums(pl, D, W, O, ck, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
     return FTCNN_OK;
 }
 

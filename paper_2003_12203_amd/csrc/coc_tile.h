@@ -1,0 +1,118 @@
+// Work that extra workgroups of the convolution launch do beside its
+// matrix-core tiles when the layer's input checksums were encoded by the
+// channels-last copy that precedes it (Sec. 3.2):
+//
+//   combine   Cd1, Cd2 = the image-split partial sums of that copy, added in
+//             split order (only when the images were split);
+//   CoC       the checksum-of-checksum products of Sec. 3.2 at every output
+//             position, Co5 = Cd1 (x) Cw1, Co6 = Cd1 (x) Cw2, Co7 = Cd2 (x) Cw1,
+//             as partial products over ranges of input channels; the final
+//             detection launch adds the ranges in order.
+//
+// A CoC workgroup owns a tile of output positions and one channel range.  For
+// each group of cc channels it stages the tile's input window of Cd1 and Cd2
+// (float64, zero outside the feature map) in LDS, then every thread evaluates
+// the R x S taps of its own position from there: each checksum element is read
+// from memory once per tile instead of once per tap.
+#pragma once
+
+#include "ftcnn_internal.h"
+
+namespace ftcnn {
+
+// Cd1 or Cd2 at element i: the image-split partials (stride apart) added in split order.
+__device__ inline double cd_at(const double *__restrict__ p, long long stride, int ns, long long i) {
+    double a = p[i];
+    for (int s = 1; s < ns; ++s) a += p[(long long)s * stride + i];
+    return a;
+}
+
+// Sources of Cd1 and Cd2 for the extra workgroups: final arrays (ns = 1) or
+// image-split partials [ns][2][Ch*H*W] (p2 = p1 + Ch*H*W, stride = 2*Ch*H*W).
+struct CdSrc {
+    const double *p1, *p2;
+    long long stride;
+    int ns;
+};
+
+// One combine workgroup: 2*NT consecutive elements of Cd1 and Cd2.
+template <int NT>
+__device__ inline void combine_block(const Geom &g, const CdSrc &src, double *__restrict__ cd1,
+                                     double *__restrict__ cd2, int blk) {
+    const long long base = (long long)blk * 2 * NT;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const long long i = base + u * NT + threadIdx.x;
+        if (i < g.CHW) {
+            cd1[i] = cd_at(src.p1, src.stride, src.ns, i);
+            cd2[i] = cd_at(src.p2, src.stride, src.ns, i);
+        }
+    }
+}
+
+// One CoC workgroup (blk < tiles * groups), using lds (2 * cc * window doubles).
+// Writes slice `group` of copart [groups][3][E*F]: this channel range's share
+// of Co5, Co6, Co7 at the tile's positions.  Each thread sums its taps in the
+// fixed order (channel, r, s).
+template <int NT>
+__device__ inline void coc_block(const Geom &g, const CocTile &ct, const CdSrc &src, const double *__restrict__ cw1,
+                                 const double *__restrict__ cw2, double *__restrict__ copart, int blk,
+                                 double *lds) {
+    const int tile = blk % ct.tiles, grp = blk / ct.tiles;
+    const int bx = tile / ct.tiles_x, by = tile - (tile / ct.tiles_x) * ct.tiles_x;
+    const int x0 = bx * ct.ty, y0 = by * ct.tx;
+    const int rows = ct.ty < g.E - x0 ? ct.ty : g.E - x0;
+    const int cols = ct.tx < g.F - y0 ? ct.tx : g.F - y0;
+    const int PH = (rows - 1) * g.U + g.R, PW = (cols - 1) * g.U + g.S;
+    const int plane = PH * PW;
+    const int c0 = (int)((long long)grp * g.C / ct.groups), c1 = (int)((long long)(grp + 1) * g.C / ct.groups);
+    const int t = threadIdx.x;
+    const int tyi = t / ct.tx, txi = t - (t / ct.tx) * ct.tx;
+    const bool mine = tyi < rows && txi < cols;
+    const int ih0 = g.U * x0 - g.P, iw0 = g.U * y0 - g.P;
+    const int RS = g.R * g.S;
+    double *s1 = lds, *s2 = lds + (size_t)ct.cc * plane;
+    double c5 = 0.0, c6 = 0.0, c7 = 0.0;
+    for (int cb = c0; cb < c1; cb += ct.cc) {
+        const int nc = ct.cc < c1 - cb ? ct.cc : c1 - cb;
+        __syncthreads();   // the previous group's window is no longer read
+        for (int e = t; e < nc * plane; e += NT) {
+            const int c = e / plane, rem = e - c * plane;
+            const int i = rem / PW, j = rem - (rem / PW) * PW;
+            const int ih = ih0 + i, iw = iw0 + j;
+            double a1 = 0.0, a2 = 0.0;
+            if ((unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W) {
+                const long long idx = ((long long)(cb + c) * g.H + ih) * g.W + iw;
+                a1 = cd_at(src.p1, src.stride, src.ns, idx);
+                a2 = cd_at(src.p2, src.stride, src.ns, idx);
+            }
+            s1[e] = a1;
+            s2[e] = a2;
+        }
+        __syncthreads();
+        if (mine) {
+            for (int c = 0; c < nc; ++c) {
+                const double *w1 = cw1 + (long long)(cb + c) * RS, *w2 = cw2 + (long long)(cb + c) * RS;
+                const double *r1 = s1 + c * plane + tyi * g.U * PW + txi * g.U;
+                const double *r2 = s2 + c * plane + tyi * g.U * PW + txi * g.U;
+                for (int r = 0; r < g.R; ++r)
+                    for (int s = 0; s < g.S; ++s) {
+                        const double d1 = r1[r * PW + s], d2 = r2[r * PW + s];
+                        const double v1 = w1[r * g.S + s], v2 = w2[r * g.S + s];
+                        c5 = fma(d1, v1, c5);
+                        c6 = fma(d1, v2, c6);
+                        c7 = fma(d2, v1, c7);
+                    }
+            }
+        }
+    }
+    if (mine) {
+        const int p = (x0 + tyi) * g.F + y0 + txi;
+        double *o = copart + (size_t)grp * 3 * g.EF + p;
+        o[0] = c5;
+        o[g.EF] = c6;
+        o[2 * (size_t)g.EF] = c7;
+    }
+}
+
+}  // namespace ftcnn

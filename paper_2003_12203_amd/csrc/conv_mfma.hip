@@ -18,6 +18,7 @@
 
 #include "ftcnn_internal.h"
 #include "encode_block.h"
+#include "coc_tile.h"
 
 namespace ftcnn {
 namespace {
@@ -361,21 +362,26 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
 // rows give sum O, sum (m + wbase) O, (n + wbase) sum O and sum O^2, written as
 // slice (tile_m * N + n) of a [slices][4][E*F] float64 array; block 0 resets the
 // report.  EPI 2: EPI 1 with faults planted in the stored values first.
-// With EPI 1 and 2 the grid may also carry workgroups that encode the input
-// checksums Cd1, Cd2 of D (Sec. 3.2) instead of a tile: groups of eight
-// consecutive workgroup ids (one per XCD) are encode groups, every
-// enc_stride-th group from the start of the grid, so that the memory-bound
-// encode runs beside the matrix-bound tiles of the same launch.
+// With EPI 1 and 2 the first aux_groups groups of eight consecutive workgroup
+// ids (one per XCD) may do other work of the protected layer instead of a tile,
+// memory-bound work that runs beside the matrix-bound tiles of the same launch:
+//   aux_kind 1: encode the input checksums Cd1, Cd2 of D (Sec. 3.2);
+//   aux_kind 2: combine the image-split partials of Cd1, Cd2 left by the
+//               channels-last copy, and compute the Co5..Co7 partial products
+//               (coc_tile.h).
 struct NoFaults {};
 template <int EPI> struct Epi {
     double *part;
     ftcnn_report *rep;
     int cap;
-    double *cd1, *cd2;
-    int enc_blocks;   // encode workgroups needed
-    int enc_groups;   // groups of eight workgroup ids given to the encode (0: none)
-    int enc_stride;   // every enc_stride-th group of eight is an encode group
-    int enc_vec;      // 16-byte loads in the encode blocks
+    int aux_kind, aux_blocks, aux_groups;
+    double *cd1, *cd2;   // kind 1: encoded here; kind 2: written by the combine workgroups
+    int enc_vec;         // kind 1: 16-byte loads
+    CdSrc src;           // kind 2
+    const double *cw1, *cw2;
+    double *copart;
+    CocTile co;
+    int co_slices;       // Co partial slices this launch writes (recorded in rep->reserved[1])
     typename std::conditional<EPI == 2, FaultList, NoFaults>::type fl;
 };
 template <> struct Epi<0> {};
@@ -407,19 +413,26 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     const int tid = threadIdx.x;
     int bid = blockIdx.x;
     if constexpr (EPI != 0) {
-        if (bid == 0 && tid == 0) reset_report(ep.rep, ep.cap);
-        if (ep.enc_groups > 0) {
-            const int grp = bid >> 3, sub = bid & 7;
-            if (grp % ep.enc_stride == ep.enc_stride - 1 && grp / ep.enc_stride < ep.enc_groups) {
-                const int eb = (grp / ep.enc_stride) * 8 + sub;
-                if (eb < ep.enc_blocks) {
-                    if (ep.enc_vec) encode_block<T, C::NT, kEncVec>(D, g, eb, ep.cd1, ep.cd2);
-                    else encode_block<T, C::NT, 1>(D, g, eb, ep.cd1, ep.cd2);
+        if (bid == 0 && tid == 0) {
+            reset_report(ep.rep, ep.cap);
+            ep.rep->reserved[1] = ep.co_slices;
+        }
+        if (ep.aux_groups > 0) {
+            if ((bid >> 3) < ep.aux_groups) {
+                if (bid < ep.aux_blocks) {
+                    if (ep.aux_kind == 1) {
+                        if (ep.enc_vec) encode_block<T, C::NT, kEncVec>(D, g, bid, ep.cd1, ep.cd2);
+                        else encode_block<T, C::NT, 1>(D, g, bid, ep.cd1, ep.cd2);
+                    } else if (bid < ep.co.comb_blocks) {
+                        combine_block<C::NT>(g, ep.src, ep.cd1, ep.cd2, bid);
+                    } else {
+                        coc_block<C::NT>(g, ep.co, ep.src, ep.cw1, ep.cw2, ep.copart, bid - ep.co.comb_blocks,
+                                         reinterpret_cast<double *>(smem));
+                    }
                 }
                 return;
             }
-            const int before = (grp + 1) / ep.enc_stride < ep.enc_groups ? (grp + 1) / ep.enc_stride : ep.enc_groups;
-            bid = (grp - before) * 8 + sub;   // keeps bid % 8, hence the XCD the tile order assumes
+            bid -= 8 * ep.aux_groups;   // keeps bid % 8, hence the XCD the tile order assumes
             if (bid >= tiles_total) return;
         }
     }
@@ -687,21 +700,24 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     Epi<EPI> e = ep;
     long long grid = total;
     if constexpr (EPI != 0) {
-        e.enc_blocks = e.enc_groups = 0;
-        e.enc_stride = 1;
-        if (e.cd1) {
+        if (e.aux_kind == 1) {
             e.enc_vec = g.CHW % kEncVec == 0 && reinterpret_cast<uintptr_t>(D) % (kEncVec * sizeof(T)) == 0;
             const long long per = (long long)C::NT * (e.enc_vec ? kEncVec : 1);
             const long long eb = (g.CHW + per - 1) / per;
-            const long long eg = (eb + 7) / 8, tg = (total + 7) / 8;
             if (eb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-            e.enc_blocks = (int)eb;
-            e.enc_groups = (int)eg;
-            // all encode groups first: they start on every CU at once and are done while the first
-            // tiles run (spreading them through the grid measured slower: late encode groups stretch
+            e.aux_blocks = (int)eb;
+        }
+        if (e.aux_kind == 2 && e.co_slices > 0 && (size_t)2 * e.co.cc * ((e.co.ty - 1) * g.U + g.R) * ((e.co.tx - 1) * g.U + g.S) *
+                                       sizeof(double) > C::LDS_BYTES)
+            return hipErrorInvalidValue;   // the plan sized the CoC window for this tile's LDS
+        if (e.aux_kind != 0 && e.aux_blocks > 0) {
+            // all extra workgroups first: they start on every CU at once and are done while the
+            // first tiles run (spreading them through the grid measured slower: late ones stretch
             // the launch, interleaved ones slow the tiles beside them)
-            e.enc_stride = 1;
-            grid = 8 * (tg + eg);
+            e.aux_groups = (e.aux_blocks + 7) / 8;
+            grid = 8 * (e.aux_groups + (total + 7) / 8);
+        } else {
+            e.aux_groups = 0;
         }
     }
     if (grid > 0x7FFFFFFFLL) return hipErrorInvalidValue;
@@ -720,6 +736,8 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
 // One tile configuration, dispatched on the weight alignment and the epilogue.
 template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     static constexpr int TM = WM * FM * 32;
+    static constexpr int NT = Cfg<Tr, WM, WP, FM, FP>::NT;
+    static constexpr size_t LDS_BYTES = Cfg<Tr, WM, WP, FM, FP>::LDS_BYTES;
     // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
     template <int EPI>
     static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep,
@@ -783,25 +801,53 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
     return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
-hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, double *cd1, double *cd2,
+void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes) {
+    with_tile(g, [&](auto t) {
+        *threads = decltype(t)::NT;
+        *lds_bytes = decltype(t)::LDS_BYTES;
+        return 0;
+    });
+}
+
+hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
                             ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
                             hipStream_t st) {
     char *w = static_cast<char *>(ws);
-    double *part = reinterpret_cast<double *>(w + pl.off_sums);
+    double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
     const void *Dc = D, *Wc = W;
+    int aux_kind = 0, aux_blocks = 0, co_slices = 0;
+    CdSrc src{cd1, cd2, 0, 1};
     if (pl.nhwc) {
-        // channels-last copies; the encode (if asked) rides in the same launch
+        // channels-last copies; the copy of D also encodes Cd1, Cd2 (if asked)
         const hipError_t e = launch_prep(pl, D, W, cd1, cd2, ws, st);
         if (e != hipSuccess) return e;
         Dc = w + pl.off_dt;
         Wc = w + pl.off_wt;
-        cd1 = cd2 = nullptr;
+        if (cd1) {
+            const int ns = pl.prep_ns;
+            if (ns > 1) {
+                const double *p1 = reinterpret_cast<const double *>(w + pl.off_encp);
+                src = CdSrc{p1, p1 + pl.g.CHW, 2 * pl.g.CHW, ns};
+            }
+            const bool coc = pl.co_in_conv && ck->cw1 && ck->cw2;
+            const int comb = ns > 1 ? pl.co.comb_blocks : 0;
+            aux_blocks = comb + (coc ? pl.co.tiles * pl.co.groups : 0);
+            aux_kind = aux_blocks > 0 ? 2 : 0;
+            co_slices = coc ? pl.co.groups : 0;
+        }
+    } else if (cd1) {
+        aux_kind = 1;   // encode workgroups; their count follows the tile's threads
     }
+    CocTile co = pl.co;
+    if (!(pl.nhwc && pl.prep_ns > 1)) co.comb_blocks = 0;
+    double *part = reinterpret_cast<double *>(w + pl.off_sums);
+    double *copart = reinterpret_cast<double *>(w + pl.off_copart);
+    const double *cw1 = ck ? ck->cw1 : nullptr, *cw2 = ck ? ck->cw2 : nullptr;
     if (nf == 0) {
-        Epi<1> ep{part, rep, cap, cd1, cd2, 0, 0, 1, 0, {}};
+        Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}};
         return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc); });
     }
-    Epi<2> ep{part, rep, cap, cd1, cd2, 0, 0, 1, 0, {}};
+    Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
     return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc); });

@@ -685,57 +685,76 @@ __device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double 
 // fixed order, then the CoC-D test) with the correction chain run in the same
 // workgroup for every position it flags.  A clean layer pays nothing for the
 // correction module, and no separate launch is needed.  With COC the same
-// lanes first compute Co5..Co7 of their position and store them.
+// lanes also produce Co5..Co7 of their position and store them: from the
+// channel-range partials the convolution launch left (rep->reserved[1] of
+// them), or else from the taps of Cd and Cw.
+//
+// TPP threads share a position, and consecutive threads take consecutive
+// positions (thread t: position t % per, lane t / per), so every load of a
+// partial slice is a coalesced run; the lanes of a position are then added by
+// a fixed tree in LDS.
 template <typename T, int TPP, bool COC>
 __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int splits, const double *__restrict__ part,
+                                                                  const double *__restrict__ copart, int max_groups,
                                                                   double *co5, double *co6, double *co7,
                                                                   double *so5, double *so6, double *so7, double *q5,
                                                                   int *__restrict__ flags, double *scratch,
                                                                   size_t stride, int nslots) {
     __shared__ Sh sh;
+    constexpr int NV = COC ? 7 : 4;
+    __shared__ double red[TPP > 1 ? NV : 1][TPP > 1 ? kThreads : 1];
     const Geom &g = c.g;
-    const int per = kThreads / TPP;
-    const int lane = threadIdx.x % TPP, slot = threadIdx.x / TPP;
+    constexpr int per = kThreads / TPP;
+    const int slot = threadIdx.x % per, lane = threadIdx.x / per;
     const int p = blockIdx.x * per + slot;
-    double c5 = 0.0, c6 = 0.0, c7 = 0.0;
-    double a = 0.0, b = 0.0, cc = 0.0, d = 0.0;
+    double v[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = 0.0;
     if (p < g.EF) {
         if constexpr (COC) {
-            const int x = p / g.F;
-            coc_taps<T, TPP>(c, lane, x, p - x * g.F, c5, c6, c7);
+            // slices written by the convolution launch that reset this report (never more than
+            // the workspace holds)
+            const int groups = min(c.rep->reserved[1], max_groups);
+            if (groups > 0) {
+                for (int s = lane; s < groups; s += TPP) {
+                    const double *ps = copart + (size_t)s * 3 * g.EF + p;
+                    v[4] += ps[0];
+                    v[5] += ps[g.EF];
+                    v[6] += ps[2 * (size_t)g.EF];
+                }
+            } else {
+                const int x = p / g.F;
+                coc_taps<T, TPP>(c, lane, x, p - x * g.F, v[4], v[5], v[6]);
+            }
         }
         for (int s = lane; s < splits; s += TPP) {
             const double *ps = part + (size_t)s * 4 * g.EF + p;
-            a += ps[0];
-            b += ps[g.EF];
-            cc += ps[2 * (size_t)g.EF];
-            d += ps[3 * (size_t)g.EF];
+            v[0] += ps[0];
+            v[1] += ps[g.EF];
+            v[2] += ps[2 * (size_t)g.EF];
+            v[3] += ps[3 * (size_t)g.EF];
         }
     }
-    if constexpr (TPP == kThreads) {
-        // one position per workgroup: waves first, then the four waves in order
-        if constexpr (COC) {
-            double v[7] = {a, b, cc, d, c5, c6, c7};
-            bsum<7>(v, sh);
-            a = v[0]; b = v[1]; cc = v[2]; d = v[3]; c5 = v[4]; c6 = v[5]; c7 = v[6];
-        } else {
-            double v[4] = {a, b, cc, d};
-            bsum<4>(v, sh);
-            a = v[0]; b = v[1]; cc = v[2]; d = v[3];
-        }
-    } else {
+    if constexpr (TPP > 1) {
 #pragma unroll
-        for (int o = TPP / 2; o > 0; o >>= 1) {
-            a += __shfl_xor(a, o, 64);
-            b += __shfl_xor(b, o, 64);
-            cc += __shfl_xor(cc, o, 64);
-            d += __shfl_xor(d, o, 64);
-            if constexpr (COC) {
-                c5 += __shfl_xor(c5, o, 64);
-                c6 += __shfl_xor(c6, o, 64);
-                c7 += __shfl_xor(c7, o, 64);
-            }
+        for (int i = 0; i < NV; ++i) red[i][threadIdx.x] = v[i];
+#pragma unroll
+        for (int h = TPP / 2; h > 0; h >>= 1) {
+            __syncthreads();
+            if (lane < h)
+#pragma unroll
+                for (int i = 0; i < NV; ++i) red[i][threadIdx.x] += red[i][threadIdx.x + h * per];
         }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < NV; ++i) v[i] = red[i][slot];
+    }
+    double a = v[0], b = v[1], cc = v[2], d = v[3];
+    double c5 = 0.0, c6 = 0.0, c7 = 0.0;
+    if constexpr (COC) {
+        c5 = v[4];
+        c6 = v[5];
+        c7 = v[6];
     }
     int flag = 0;
     if (p < g.EF && lane == 0) {
@@ -826,11 +845,17 @@ hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, cons
     const double *part = reinterpret_cast<const double *>(w + off_part);
     int *flags = reinterpret_cast<int *>(w + pl.off_flags);
     double *scratch = reinterpret_cast<double *>(w + pl.off_corr);
-    const int tpp = final_tpp(sp, coc ? pl.g.K : 0, pl.g.EF);
+    // Co5..Co7 of a channels-last layer come as partial slices from the convolution launch
+    // (the kernel checks rep->reserved[1] and falls back to the taps)
+    const int taps = coc ? (pl.co_in_conv ? pl.co.groups : pl.g.K) : 0;
+    const int tpp = final_tpp(sp, taps, pl.g.EF);
+    const double *copart = reinterpret_cast<const double *>(w + pl.off_copart);
+    const int max_groups = pl.co_in_conv ? pl.co.groups : 0;
     const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
-#define VC(TPP, COC)                                                                                       \
-    verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, ck.co5, ck.co6, ck.co7,   \
-                                                                    ck.so5, ck.so6, ck.so7, ck.q5, flags,   \
+#define VC(TPP, COC)                                                                                            \
+    verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, copart, max_groups, ck.co5,       \
+                                                                    ck.co6, ck.co7,                              \
+                                                                    ck.so5, ck.so6, ck.so7, ck.q5, flags,        \
                                                                     scratch, pl.corr_stride, pl.corr_slots)
     if (coc) {
         if (tpp == 1) VC(1, true);

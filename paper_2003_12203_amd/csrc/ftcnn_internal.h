@@ -23,6 +23,19 @@ struct Geom {
     int dtype, wbase;
 };
 
+// Tiling of the Co5..Co7 products computed by extra workgroups of the
+// convolution launch (channels-last layers): output tiles of tx columns (of F)
+// by ty rows (of E), cc channels staged in LDS per step, the channels split
+// into `groups` ranges; comb_blocks workgroups combine the image-split
+// partials of Cd1, Cd2 when ns > 1.
+struct CocTile {
+    int tx, ty, cc;
+    int tiles_x, tiles;
+    int groups;
+    int comb_blocks;
+    int ns;
+};
+
 // Split counts and workspace offsets shared by every call on one layer.
 struct Plan {
     Geom g;
@@ -33,11 +46,15 @@ struct Plan {
     int corr_slots;                   // per-workgroup scratch slices (correction or fused verification)
     int sum_splits;                   // partial-sum slices written by the convolution epilogue
     bool nhwc;                        // the convolution reads channels-last copies of D and W
-    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, bytes;
+    int prep_ns;                      // image ranges of the encode fused into the channels-last copy
+    bool co_in_conv;                  // Co5..Co7 partials computed by workgroups of the convolution launch
+    CocTile co;                       // their tiling (co_in_conv)
+    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
 
 constexpr int kThreads = 256;
+constexpr int kPrepBatch = 8;   // images per load round of the channels-last copy
 constexpr int kMaxFaults = 64;
 constexpr double kUAcc = 5.9604644775390625e-08;   // 2^-24, fp32 accumulation unit roundoff
 constexpr double kUOutBf16 = 3.90625e-03;          // 2^-8, bf16 storage unit roundoff
@@ -114,18 +131,26 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
 // The convolution with the CoC-D summations in its epilogue: every tile also
 // writes its (So5, So6, So7, sum of squares) partials for the pixels it owns to
 // the workspace (pl.sum_splits slices, layout of the verification partials) and
-// the report is reset.  With cd1 and cd2 set, extra workgroups of the same
-// launch encode Cd1, Cd2 of D.  faults (at most kMaxFaults, host array) are
-// planted in the stored values before they are summed.
-hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, double *cd1, double *cd2,
+// the report is reset.  With ck->cd1 and cd2 set, Cd1 and Cd2 are encoded in
+// the same pass (by the channels-last copy, or by extra workgroups of the
+// convolution launch); on pl.co_in_conv layers with ck->cw1 and cw2 set too,
+// extra workgroups of the convolution launch also compute the Co5..Co7
+// partials (pl.co.groups slices at pl.off_copart), and rep->reserved[1] records
+// how many.  faults (at most kMaxFaults, host array) are planted in the stored
+// values before they are summed.
+hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
                             ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
                             hipStream_t st);
 // Rows of C per workgroup tile of the convolution chosen for this layer.
 int conv_tile_m(const Geom &g);
+// Threads per workgroup and dynamic LDS bytes of the convolution chosen for this layer.
+void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes);
 // Layers whose convolution reads channels-last copies (pl.nhwc): Ch a multiple of 32.
 inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0; }
 // Dt = D in [n][h][w][c] order and Wt = W in [m][r][s][c] order into the workspace
-// (pl.off_dt, pl.off_wt); with cd1 and cd2 set, the same launch encodes them.
+// (pl.off_dt, pl.off_wt); with cd1 and cd2 set, the copy of D also encodes them
+// (directly when pl.prep_ns == 1, else as image-split partials at pl.off_encp
+// that the convolution launch combines into cd1 and cd2).
 hipError_t launch_prep(const Plan &pl, const void *D, const void *W, double *cd1, double *cd2, void *ws,
                        hipStream_t st);
 // The convolution alone through the path ftcnn_conv_fwd_sums takes (channels-last
@@ -153,15 +178,14 @@ hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void 
 // Threads that share one position in the final verification stage (1, 4, 16,
 // 64 or a whole workgroup; the float64 split partials of that position, and the
 // K taps of its Co5..Co7 when those are computed there too, are spread over
-// them): enough lanes for the work of one position, but no more than keeps the
-// whole grid to about two million threads.
+// them): at most about 24 partial rows or taps per thread, and enough threads
+// in the grid (32K) to keep every CU's loads in flight.
 inline int final_tpp(int splits, int taps, long long positions) {
     const long long w = (long long)splits + taps;
     int t = 1;
-    while (t < kThreads && 2LL * t < w) t *= 4;
-    if (t > kThreads) t = kThreads;
-    while (t > 1 && (long long)t * positions > (2LL << 20)) t /= 4;
-    return t;
+    while (t < kThreads && w > 24LL * t) t *= 4;
+    while (t < kThreads && (long long)t * positions < 32768) t *= 4;
+    return t > kThreads ? kThreads : t;
 }
 hipError_t launch_inject(const Plan &pl, void *O, const ftcnn_fault *f, int nf, hipStream_t st);
 

@@ -2,47 +2,94 @@
 // tensors as eq. (1) uses, in another order,
 //   Dt[n][h][w][c] = D[n][c][h][w],   Wt[m][r][s][c] = W[m][c][r][s],
 // so that the K = (r, s, c) run of one pixel is contiguous in memory and the
-// im2col gather becomes 16-byte loads.  Workgroups of the same launch can also
-// encode the input checksums Cd1, Cd2 of D (Sec. 3.2), which read D in its own
-// order.  Pure data movement: no value is changed.
+// im2col gather becomes 16-byte loads.
+//
+// The copy of D also encodes the input checksums of Sec. 3.2,
+//   Cd1 = sum_n D_n,   Cd2 = sum_n (n + wbase) D_n,
+// from the values it moves, so D is read once for both.  A workgroup owns a
+// 32-channel x 32-position tile of the feature maps and walks a range of
+// images in order, keeping the running float64 sums of its tile in registers;
+// layers with few tiles split the images into ranges (one partial pair per
+// range, combined in a fixed order by the convolution launch that follows).
 #include "ftcnn_internal.h"
-#include "encode_block.h"
 
 namespace ftcnn {
 namespace {
 
 constexpr int TT = 32;   // transpose tile: 32 channels x 32 positions, through LDS
 
-template <typename T>
+template <typename T> __device__ inline double widen(T v) {
+    if constexpr (sizeof(T) == 4) return (double)v;
+    else return (double)bf16_bits_to_f32(v);
+}
+
+template <typename T, bool ENC>
 __global__ __launch_bounds__(kThreads) void prep_kernel(const T *__restrict__ D, const T *__restrict__ W,
                                                         T *__restrict__ Dt, T *__restrict__ Wt, Geom g,
-                                                        double *cd1, double *cd2, int enc_blocks, int enc_vec,
-                                                        int tr_blocks, int hw_tiles, int c_tiles) {
-    __shared__ T tile[TT][TT + 1];
+                                                        double *cd1, double *cd2, long long split_stride,
+                                                        int tr_blocks, int hw_tiles, int c_tiles, int ns) {
+    __shared__ T tile[kPrepBatch][TT][TT + 1];
     int b = blockIdx.x;
-    if (b < enc_blocks) {
-        if (enc_vec) encode_block<T, kThreads, kEncVec>(D, g, b, cd1, cd2);
-        else encode_block<T, kThreads, 1>(D, g, b, cd1, cd2);
-        return;
-    }
-    b -= enc_blocks;
     const int HW = g.H * g.W;
     if (b < tr_blocks) {
-        const int ht = b % hw_tiles, rest = b / hw_tiles;
-        const int ct = rest % c_tiles, n = rest / c_tiles;
+        const int tiles = hw_tiles * c_tiles;
+        const int split = b / tiles, rest = b - split * tiles;
+        const int ht = rest % hw_tiles, ct = rest / hw_tiles;
+        const int n0 = (int)((long long)split * g.N / ns), n1 = (int)((long long)(split + 1) * g.N / ns);
         const int tx = threadIdx.x % TT, ty = threadIdx.x / TT;   // 32 x 8 threads
-        const T *src = D + (long long)n * g.CHW;
+        const int hw_in = ht * TT + tx;                            // this thread's load column
+        const bool in_ok = hw_in < HW;
+        const T *src = D + (long long)(ct * TT + ty) * HW + (in_ok ? hw_in : 0);
+        double a1[TT / 8], a2[TT / 8];
 #pragma unroll
-        for (int q = 0; q < TT / 8; ++q) {   // rows of channels, coalesced along h*w
-            const int c = ct * TT + ty + 8 * q, hw = ht * TT + tx;
-            tile[ty + 8 * q][tx] = hw < HW ? src[(long long)c * HW + hw] : T(0);
+        for (int q = 0; q < TT / 8; ++q) a1[q] = a2[q] = 0.0;
+        // kPrepBatch images per round: all their loads in flight at once, one LDS tile each
+        for (int nb = n0; nb < n1; nb += kPrepBatch) {
+            T v[kPrepBatch][TT / 8];
+#pragma unroll
+            for (int j = 0; j < kPrepBatch; ++j) {
+                const int n = nb + j < n1 ? nb + j : n1 - 1;   // a short last round re-reads a row it ignores
+#pragma unroll
+                for (int q = 0; q < TT / 8; ++q) v[j][q] = src[(long long)n * g.CHW + (long long)(8 * q) * HW];
+            }
+            if (nb > n0) __syncthreads();   // the previous round's tiles are read
+#pragma unroll
+            for (int j = 0; j < kPrepBatch; ++j) {
+                if (nb + j >= n1) break;
+                if constexpr (ENC) {
+                    const double wgt = (double)(nb + j + g.wbase);
+#pragma unroll
+                    for (int q = 0; q < TT / 8; ++q) {
+                        const double x = widen(v[j][q]);
+                        a1[q] += x;
+                        a2[q] = fma(wgt, x, a2[q]);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < TT / 8; ++q) tile[j][ty + 8 * q][tx] = v[j][q];
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kPrepBatch; ++j) {
+                if (nb + j >= n1) break;
+                T *dst = Dt + (long long)(nb + j) * g.CHW;
+#pragma unroll
+                for (int q = 0; q < TT / 8; ++q) {   // rows of positions, coalesced along c
+                    const int hw = ht * TT + ty + 8 * q;
+                    if (hw < HW) dst[(long long)hw * g.C + ct * TT + tx] = tile[j][tx][ty + 8 * q];
+                }
+            }
         }
-        __syncthreads();
-        T *dst = Dt + (long long)n * g.CHW;
+        if constexpr (ENC) {
+            if (in_ok) {
+                double *o1 = cd1 + (long long)split * split_stride, *o2 = cd2 + (long long)split * split_stride;
 #pragma unroll
-        for (int q = 0; q < TT / 8; ++q) {   // rows of positions, coalesced along c
-            const int hw = ht * TT + ty + 8 * q, c = ct * TT + tx;
-            if (hw < HW) dst[(long long)hw * g.C + c] = tile[tx][ty + 8 * q];
+                for (int q = 0; q < TT / 8; ++q) {
+                    const long long col = (long long)(ct * TT + ty + 8 * q) * HW + hw_in;
+                    o1[col] = a1[q];
+                    o2[col] = a2[q];
+                }
+            }
         }
         return;
     }
@@ -61,22 +108,31 @@ hipError_t run(const Plan &pl, const void *D, const void *W, double *cd1, double
     char *w = static_cast<char *>(ws);
     T *Dt = reinterpret_cast<T *>(w + pl.off_dt);
     T *Wt = reinterpret_cast<T *>(w + pl.off_wt);
-    long long enc = 0;
-    int enc_vec = 0;
-    if (cd1) {
-        enc_vec = g.CHW % kEncVec == 0 && reinterpret_cast<uintptr_t>(D) % (kEncVec * sizeof(T)) == 0;
-        const long long per = (long long)kThreads * (enc_vec ? kEncVec : 1);
-        enc = (g.CHW + per - 1) / per;
-    }
     const long long HW = (long long)g.H * g.W;
     const long long hw_tiles = (HW + TT - 1) / TT, c_tiles = g.C / TT;
-    const long long tr = (long long)g.N * c_tiles * hw_tiles;
+    // without the encode every round of images is a workgroup of its own
+    const int ns = cd1 ? pl.prep_ns : (g.N + kPrepBatch - 1) / kPrepBatch;
+    const long long tr = (long long)ns * c_tiles * hw_tiles;
     const long long wb = ((long long)g.M * g.K + kThreads - 1) / kThreads;
-    const long long grid = enc + tr + wb;
+    const long long grid = tr + wb;
     if (grid > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    prep_kernel<T><<<(unsigned)grid, kThreads, 0, st>>>(static_cast<const T *>(D), static_cast<const T *>(W), Dt, Wt,
-                                                        g, cd1, cd2, (int)enc, enc_vec, (int)tr, (int)hw_tiles,
-                                                        (int)c_tiles);
+    double *o1 = cd1, *o2 = cd2;
+    long long stride = 0;
+    if (cd1 && ns > 1) {
+        // image-split partials [ns][2][Ch*H*W], combined by the convolution launch
+        o1 = reinterpret_cast<double *>(w + pl.off_encp);
+        o2 = o1 + g.CHW;
+        stride = 2 * g.CHW;
+    }
+    if (cd1)
+        prep_kernel<T, true><<<(unsigned)grid, kThreads, 0, st>>>(static_cast<const T *>(D), static_cast<const T *>(W),
+                                                                  Dt, Wt, g, o1, o2, stride, (int)tr, (int)hw_tiles,
+                                                                  (int)c_tiles, ns);
+    else
+        prep_kernel<T, false><<<(unsigned)grid, kThreads, 0, st>>>(static_cast<const T *>(D),
+                                                                   static_cast<const T *>(W), Dt, Wt, g, nullptr,
+                                                                   nullptr, 0, (int)tr, (int)hw_tiles, (int)c_tiles,
+                                                                   ns);
     return hipGetLastError();
 }
 
