@@ -66,7 +66,9 @@ struct Cfg {
     static constexpr int KG = NT / TP;                               // threads per pixel along k
     static constexpr int KR = TK / KG;                               // k per thread in the gather
     static_assert(NT % TP == 0 && TK % KG == 0 && KR % VEC == 0, "tile shape");
-    static_assert(KR <= 32 && A_PER * VEC <= 32, "gather masks are 32-bit");
+    static_assert(KR <= 64 && A_PER * VEC <= 64, "gather masks are at most 64-bit");
+    // one bit per gathered element of a thread
+    using Mask = typename std::conditional<(KR > 32 || A_PER * VEC > 32), uint64_t, uint32_t>::type;
     static constexpr size_t LDS_BYTES = 2ull * (TM + TP) * LDK * sizeof(T);
     static_assert(LDS_BYTES <= 160 * 1024, "tile exceeds the LDS of a CU");
 };
@@ -101,9 +103,10 @@ __device__ inline void a_slots(const Geom &g, int m0, int tid, ASlots<C> &as) {
 // The masks are applied only when the registers go to LDS (after the MFMAs of
 // the current chunk), so no wait for these loads sits in front of the MFMAs.
 template <typename C>
-__device__ inline uint32_t load_a(const typename C::T *__restrict__ Wt, const Geom &g, int kbase, bool,
-                                  const ASlots<C> &as, Pack<typename C::T, C::VEC> (&ra)[C::A_PER]) {
-    uint32_t mask = 0;
+__device__ inline typename C::Mask load_a(const typename C::T *__restrict__ Wt, const Geom &g, int kbase, bool,
+                                          const ASlots<C> &as, Pack<typename C::T, C::VEC> (&ra)[C::A_PER]) {
+    using M = typename C::Mask;
+    M mask = 0;
 #pragma unroll
     for (int i = 0; i < C::A_PER; ++i) {
         const int k = kbase + as.kq[i];
@@ -113,13 +116,13 @@ __device__ inline uint32_t load_a(const typename C::T *__restrict__ Wt, const Ge
             const bool ok = (as.base[i] >= 0) & (k < g.K);
             const uint4 *w4 = reinterpret_cast<const uint4 *>(Wt);
             ra[i].q = w4[ok ? (as.base[i] + kbase) / C::VEC : 0];
-            mask |= (ok ? ((1u << C::VEC) - 1u) : 0u) << (i * C::VEC);
+            mask |= (ok ? ((M(1) << C::VEC) - M(1)) : M(0)) << (i * C::VEC);
         } else {
 #pragma unroll
             for (int v = 0; v < C::VEC; ++v) {
                 const bool ok = (as.base[i] >= 0) & (k + v < g.K);
                 ra[i].e[v] = Wt[ok ? as.base[i] + kbase + v : 0];
-                mask |= (ok ? 1u : 0u) << (i * C::VEC + v);
+                mask |= (ok ? M(1) : M(0)) << (i * C::VEC + v);
             }
         }
     }
@@ -130,10 +133,11 @@ __device__ inline uint32_t load_a(const typename C::T *__restrict__ Wt, const Ge
 // ih0*W + iw0); the run of KR consecutive k is the same for the whole wave, so
 // (c, r, s) and the k part of the offset live in scalar registers.
 template <typename C>
-__device__ inline uint32_t load_b(const typename C::T *__restrict__ Dt, const Geom &g, int kstart_lane,
-                                  bool pvalid, int lane_base, int ih0, int iw0,
-                                  Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
-    uint32_t mask = 0;
+__device__ inline typename C::Mask load_b(const typename C::T *__restrict__ Dt, const Geom &g, int kstart_lane,
+                                          bool pvalid, int lane_base, int ih0, int iw0,
+                                          Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+    using M = typename C::Mask;
+    M mask = 0;
     using T = typename C::T;
     const int kstart = __builtin_amdgcn_readfirstlane(kstart_lane);
     const int RS = g.R * g.S;
@@ -151,7 +155,7 @@ __device__ inline uint32_t load_b(const typename C::T *__restrict__ Dt, const Ge
         const bool ok = pvalid & (kstart + j < g.K) & ((unsigned)ih < (unsigned)g.H) &
                         ((unsigned)iw < (unsigned)g.W);
         rb[j / C::VEC].e[j % C::VEC] = Dt[ok ? lane_base + koff : 0];
-        mask |= (ok ? 1u : 0u) << j;
+        mask |= (ok ? M(1) : M(0)) << j;
         // advance (c, r, s) by one k with selects (scalar registers)
         ++s;
         ++koff;
@@ -169,8 +173,8 @@ __device__ inline uint32_t load_b(const typename C::T *__restrict__ Dt, const Ge
 
 template <typename C>
 __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
-                                 Pack<typename C::T, C::VEC> (&ra)[C::A_PER], uint32_t amask,
-                                 Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC], uint32_t bmask,
+                                 Pack<typename C::T, C::VEC> (&ra)[C::A_PER], typename C::Mask amask,
+                                 Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC], typename C::Mask bmask,
                                  int bp, int bkg) {
     using T = typename C::T;
 #pragma unroll
@@ -179,7 +183,7 @@ __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
         if (C::A_SLOTS % C::NT == 0 || slot < C::A_SLOTS) {
 #pragma unroll
             for (int v = 0; v < C::VEC; ++v)
-                ra[i].e[v] = ((amask >> (i * C::VEC + v)) & 1u) ? ra[i].e[v] : T(0);
+                ra[i].e[v] = ((amask >> (i * C::VEC + v)) & 1) ? ra[i].e[v] : T(0);
             const int row = slot / (C::TK / C::VEC);
             const int kq = slot % (C::TK / C::VEC);
             *reinterpret_cast<uint4 *>(&As[row * C::LDK + kq * C::VEC]) = ra[i].q;
@@ -187,7 +191,7 @@ __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
     }
 #pragma unroll
     for (int j = 0; j < C::KR; ++j)
-        rb[j / C::VEC].e[j % C::VEC] = ((bmask >> j) & 1u) ? rb[j / C::VEC].e[j % C::VEC] : T(0);
+        rb[j / C::VEC].e[j % C::VEC] = ((bmask >> j) & 1) ? rb[j / C::VEC].e[j % C::VEC] : T(0);
 #pragma unroll
     for (int j = 0; j < C::KR; j += C::VEC)
         *reinterpret_cast<uint4 *>(&Bs[bp * C::LDK + bkg * C::KR + j]) = rb[j / C::VEC].q;
@@ -261,7 +265,7 @@ __device__ inline void mma_chunk(const typename C::T *As, const typename C::T *B
 // the chunk), so it is KR contiguous elements of one input pixel, loaded as
 // 16-byte units; the padding test is one test for the whole run.
 template <typename C>
-__device__ inline uint32_t load_b_nhwc(const typename C::T *__restrict__ Dt, const Geom &g, int kstart_lane,
+__device__ inline typename C::Mask load_b_nhwc(const typename C::T *__restrict__ Dt, const Geom &g, int kstart_lane,
                                        bool pvalid, int img_base, int ih0, int iw0,
                                        Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
     const int kstart = __builtin_amdgcn_readfirstlane(kstart_lane);
@@ -273,7 +277,8 @@ __device__ inline uint32_t load_b_nhwc(const typename C::T *__restrict__ Dt, con
     const uint4 *src = reinterpret_cast<const uint4 *>(Dt + base);
 #pragma unroll
     for (int i = 0; i < C::KR / C::VEC; ++i) rb[i].q = src[i];
-    constexpr uint32_t all = C::KR == 32 ? 0xFFFFFFFFu : ((1u << C::KR) - 1u);
+    using M = typename C::Mask;
+    constexpr M all = C::KR == 8 * (int)sizeof(M) ? ~M(0) : ((M(1) << C::KR) - M(1));
     return ok ? all : 0u;
 }
 
@@ -281,7 +286,7 @@ __device__ inline uint32_t load_b_nhwc(const typename C::T *__restrict__ Dt, con
 // time between MFMAs: (c, r, s) and the k offset advance in scalar registers.
 template <typename C> struct BGather {
     int kstart, c, r, s, koff;
-    uint32_t mask;
+    typename C::Mask mask;
     __device__ inline void begin(const Geom &g, int kstart_lane) {
         kstart = __builtin_amdgcn_readfirstlane(kstart_lane);
         const int RS = g.R * g.S;
@@ -298,7 +303,7 @@ template <typename C> struct BGather {
         const bool ok = pvalid & (kstart + j < g.K) & ((unsigned)ih < (unsigned)g.H) &
                         ((unsigned)iw < (unsigned)g.W);
         rb[j / C::VEC].e[j % C::VEC] = Dt[ok ? lane_base + koff : 0];
-        mask |= (ok ? 1u : 0u) << j;
+        mask |= (ok ? typename C::Mask(1) : typename C::Mask(0)) << j;
         ++s;
         ++koff;
         const bool ws = s == g.S;
@@ -320,7 +325,7 @@ template <typename C, int FM, int FP, bool NEXT>
 __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int arow0, int brow0,
                                  floatx16 (&acc)[FM][FP], const typename C::T *__restrict__ Dt,
                                  const typename C::T *__restrict__ Wt, const Geom &g, int kb_next, bool kvec,
-                                 const ASlots<C> &as, Pack<typename C::T, C::VEC> (&ra)[C::A_PER], uint32_t &amask,
+                                 const ASlots<C> &as, Pack<typename C::T, C::VEC> (&ra)[C::A_PER], typename C::Mask &amask,
                                  BGather<C> &bg, int bkg, bool pvalid, int lane_base, int ih0, int iw0,
                                  Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
     constexpr int TK = C::TK, LDK = C::LDK, STEPS = TK / 2;
@@ -476,14 +481,41 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     Pack<T, C::VEC> ra[C::A_PER];
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
-    uint32_t amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
-    uint32_t bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
+    typename C::Mask amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
+    typename C::Mask bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
                           : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
     store_lds<C>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
     __syncthreads();
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    if constexpr (NHWC) {
+    if constexpr (NHWC && WEAVE == 2) {
+        // channels-last, two chunks in flight: chunk kc + 2 is loaded into one register set
+        // while chunk kc is consumed from LDS, and chunk kc + 1 (loaded a whole chunk earlier,
+        // in the other set) then goes to the other LDS buffer, so the stores wait only on loads
+        // issued two chunks back.  Unrolled by two so that each register set keeps its
+        // registers; loads past the last chunk are fully masked (in-bounds, no effect).
+        Pack<T, C::VEC> ra2[C::A_PER];
+        Pack<T, C::VEC> rb2[C::KR / C::VEC];
+        typename C::Mask amask2 = load_a<C>(Wt, g, C::TK, KVEC, as, ra2);
+        typename C::Mask bmask2 = load_b_nhwc<C>(D, g, C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
+        T *A0 = As0, *A1 = As0 + C::TM * C::LDK, *B0 = Bs0, *B1 = Bs0 + C::TP * C::LDK;
+        // no exit inside the body (a chunk past the end is stored as zeros and never used), so the
+        // accumulators stay in one set of registers
+        int kc = 0;
+        for (; kc + 1 < nchunks; kc += 2) {
+            amask = load_a<C>(Wt, g, (kc + 2) * C::TK, KVEC, as, ra);
+            bmask = load_b_nhwc<C>(D, g, (kc + 2) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+            mma_chunk<C, FM, FP>(A0, B0, lane, arow0, brow0, acc);
+            store_lds<C>(A1, B1, tid, ra2, amask2, rb2, bmask2, bp, bkg);
+            __syncthreads();
+            amask2 = load_a<C>(Wt, g, (kc + 3) * C::TK, KVEC, as, ra2);
+            bmask2 = load_b_nhwc<C>(D, g, (kc + 3) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
+            mma_chunk<C, FM, FP>(A1, B1, lane, arow0, brow0, acc);
+            store_lds<C>(A0, B0, tid, ra, amask, rb, bmask, bp, bkg);
+            __syncthreads();
+        }
+        if (kc < nchunks) mma_chunk<C, FM, FP>(A0, B0, lane, arow0, brow0, acc);   // odd count: the last chunk
+    } else if constexpr (NHWC) {
         // channels-last: a whole chunk's gather is a few 16-byte loads per thread, issued
         // before this chunk's MFMAs and stored after them
         for (int kc = 0; kc + 1 < nchunks; ++kc) {
@@ -506,7 +538,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         // keeps its registers; chunks past the last one are fully masked (zeros, no effect).
         Pack<T, C::VEC> ra2[C::A_PER];
         Pack<T, C::VEC> rb2[C::KR / C::VEC];
-        uint32_t amask2 = load_a<C>(Wt, g, C::TK, KVEC, as, ra2);
+        typename C::Mask amask2 = load_a<C>(Wt, g, C::TK, KVEC, as, ra2);
         BGather<C> bg, bg2;
         bg2.mask = load_b<C>(D, g, C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
         const float *A0 = reinterpret_cast<const float *>(As0), *A1 = A0 + C::TM * C::LDK;
@@ -623,16 +655,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                 const double wm = (double)m + wb;
 #pragma unroll
                 for (int j = 0; j < FP; ++j) {
-                    typename Bt::B b = Bt::make(acc[i][j][e]);
-                    if constexpr (EPI == 2) {
-                        if (planted) {
-                            for (int f = 0; f < ep.fl.n; ++f) {
-                                const ftcnn_fault &q = ep.fl.f[f];
-                                const long long pf = (long long)q.n * g.EF + (long long)q.x * g.F + q.y;
-                                if (q.m == m && pf == pcol[j]) b = fault_apply(b, q);
-                            }
-                        }
-                    }
+                    const typename Bt::B b = Bt::make(acc[i][j][e]);
                     if (cval[j] && mok) {
                         const double v = (double)Bt::value(b);
                         s1[j] += v;
@@ -683,6 +706,31 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                 dst[g.EF] = s6;
                 dst[2 * (size_t)g.EF] = ((double)n + wb) * s1;
                 dst[3 * (size_t)g.EF] = sq;
+            }
+        }
+        if constexpr (EPI == 2) {
+            // the planted faults of this tile, in list order, on the values as stored: each one
+            // rewrites its element of O and moves the tile's partial sums of that pixel by the
+            // change it made (one thread, after every store of the tile is done)
+            if (planted) {
+                __syncthreads();
+                if (tid == 0) {
+                    for (int f = 0; f < ep.fl.n; ++f) {
+                        const ftcnn_fault &q = ep.fl.f[f];
+                        const long long pf = (long long)q.n * g.EF + (long long)q.x * g.F + q.y;
+                        if (!(q.m >= m0 && q.m < m0 + C::TM && pf >= p0 && pf < p0 + C::TP)) continue;
+                        const long long pos = pf - (long long)q.n * g.EF;
+                        T *o = O + ((long long)q.n * g.M + q.m) * g.EF + pos;
+                        const typename Bt::B b = *o, b2 = fault_apply(b, q);
+                        *o = b2;
+                        const double v = (double)Bt::value(b), v2 = (double)Bt::value(b2), d = v2 - v;
+                        double *dst = ep.part + ((size_t)mt * g.N + q.n) * 4 * g.EF + pos;
+                        dst[0] += d;
+                        dst[g.EF] += ((double)q.m + wb) * d;
+                        dst[2 * (size_t)g.EF] += ((double)q.n + wb) * d;
+                        dst[3 * (size_t)g.EF] += v2 * v2 - v * v;
+                    }
+                }
             }
         }
     }
@@ -752,9 +800,10 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
 // Tile choice per layer, from sweeps over the workload shapes on MI355X.  The
 // filter tile follows M so small-M layers waste no MFMA rows; for larger M the
 // biggest tile that still leaves about two workgroups per CU wins.  For bf16
-// (eight times the fp32 matrix rate per instruction) layers with many pixel
-// tiles take 256-row filter tiles, and the others a 64 x 128 tile with
-// 64-deep chunks (fewer barriers per flop; needs Ch % 64 == 0 channels-last).
+// (eight times the fp32 matrix rate per instruction) the channels-last loop
+// keeps two chunks in flight (WEAVE 2): 64 x 256 tiles for M <= 64, 256 x 256
+// tiles (a 128 x 128 block per wave) where there are enough of them, and
+// 128 x 128 tiles with 64-deep chunks elsewhere.
 long long n_tiles(const Geom &g, int tm, int tp) {
     return ((g.P_total + tp - 1) / tp) * (long long)((g.M + tm - 1) / tm);
 }
@@ -765,11 +814,10 @@ using F32_M96 = Tile<F32T<16>, 1, 4, 3, 2, true>;
 using F32_128x128 = Tile<F32T<16>, 2, 2, 2, 2, true>;
 using F32_128x64 = Tile<F32T<32>, 2, 2, 2, 1, true>;
 using F32_64x64 = Tile<F32T<32>, 2, 2, 1, 1, true>;
-using BF16_M32 = Tile<BF16T<32>, 1, 4, 1, 2, false>;
-using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, false>;
-using BF16_128x128 = Tile<BF16T<32>, 2, 2, 2, 2, false>;
-using BF16_256x128 = Tile<BF16T<32>, 4, 2, 2, 2, false>;
-using BF16_64x128_K64 = Tile<BF16T<64>, 2, 2, 1, 2, false>;
+using BF16_M32 = Tile<BF16T<32>, 1, 4, 1, 2, 0>;
+using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, 2>;
+using BF16_128x128_K64 = Tile<BF16T<64>, 2, 2, 2, 2, 2>;
+using BF16_256x256 = Tile<BF16T<32>, 2, 2, 4, 4, 2>;
 
 // Calls f(TileType{}) for the tile this layer uses.
 template <typename Fn>
@@ -784,10 +832,8 @@ auto with_tile(const Geom &g, Fn &&f) {
     }
     if (g.M <= 32) return f(BF16_M32{});
     if (g.M <= 64) return f(BF16_M64{});
-    if (g.M <= 128) return f(BF16_128x128{});
-    if (n_tiles(g, 256, 128) >= 192) return f(BF16_256x128{});
-    if (g.C % 64 == 0) return f(BF16_64x128_K64{});
-    return f(BF16_128x128{});
+    if (g.M >= 256 && n_tiles(g, 256, 256) >= 192) return f(BF16_256x256{});
+    return f(BF16_128x128_K64{});
 }
 
 }  // namespace

@@ -216,3 +216,111 @@ def test_protected_conv_single_call(li):
     Q = two["q5"]
     for k in ("so5", "so6", "so7"):
         np.testing.assert_allclose(one[k], two[k], rtol=0, atol=1e-12 * float(Q.max()) * max(spec.n, spec.m))
+
+
+# Layers with many images and few 32 x 32 feature-map tiles: the channels-last copy encodes Cd1,
+# Cd2 over several image ranges, the convolution launch combines them and computes the Co5..Co7
+# partials from them (ranges of 16 images in fp32, 32 in bf16; uneven ranges with n = 50).
+SPLIT_SHAPES = [
+    # n, ch, h, m, r, stride, pad, dtype
+    (64, 32, 9, 40, 3, 1, 1, "f32"),
+    (50, 32, 10, 24, 3, 2, 1, "f32"),
+    (40, 64, 5, 16, 1, 1, 0, "f32"),
+    (64, 64, 7, 48, 3, 1, 1, "bf16"),
+    (96, 64, 6, 70, 3, 2, 1, "bf16"),
+]
+
+
+def _split_spec(shape):
+    n, ch, h, m, r, u, p, dtype = shape
+    return wl.LayerSpec("split", n, ch, h, h, m, r, r, u, p, dtype)
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "n{}-c{}-h{}-m{}-r{}-u{}-{}".format(*s[:6], s[7]))
+def test_image_split_encode_integer_exact(shape):
+    """Integer data: the combined image-range partials are exactly Cd1, Cd2, and the Co5..Co7
+    partial products of the convolution launch add up exactly to the summations of O."""
+    spec = _split_spec(shape)
+    D, W = wl.gen_int_d(spec, 11), wl.gen_int_w(spec, 11)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
+    lay.encode_weights(Wd)
+    O_ref = lay.empty_output()
+    lay.conv_ws(Dd, Wd, O_ref)
+    O = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O, encode=True)
+    lay.verify_correct_sums(Dd, Wd, O, coc=True)
+    torch.cuda.synchronize()
+    iv = torch.int16 if spec.dtype == "bf16" else torch.int32
+    assert torch.equal(O.view(iv), O_ref.view(iv))
+    b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
+    cd1, cd2 = wf.encode(D, 0)
+    np.testing.assert_array_equal(b["cd1"], cd1.ravel())
+    np.testing.assert_array_equal(b["cd2"], cd2.ravel())
+    ck = wf.Checksums(cd1, cd2, *wf.encode(W, 0))
+    wf.coc_checksums(ck, spec.stride, spec.pad)
+    for name, ref in [("co5", ck.co5), ("co6", ck.co6), ("co7", ck.co7)]:
+        np.testing.assert_array_equal(b[name].reshape(ref.shape), ref)
+    if spec.dtype == "f32" or np.abs(host(O)).max() <= 256:
+        for k in ("5", "6", "7"):
+            np.testing.assert_array_equal(b["co" + k], b["so" + k])
+    assert not lay.read_report().detected
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "n{}-c{}-h{}-m{}-r{}-u{}-{}".format(*s[:6], s[7]))
+def test_image_split_decisions_match_oracle(shape):
+    """Random data with two planted faults (different positions): Cd, Co5..Co7 match the oracle,
+    and the decisions and repairs are the oracle's on the same faulted output."""
+    spec = _split_spec(shape)
+    cfg = wl.Config(93, "split", (spec,), "uniform", "he")
+    D, W = wl.gen_d(cfg, 0, spec), wl.gen_w(cfg, 0, spec)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
+    lay.encode_weights(Wd)
+    E, F = lay.E, lay.F
+    faults = [wf.Fault(spec.n - 1, spec.m - 1, E - 1, F - 1, "add", value=1.0e5),
+              wf.Fault(spec.n // 2, 1, 0, F // 2, "add", value=-2.0e5)]
+    O = lay.empty_output()
+    lay.conv_sums(Dd, Wd, O, to_ft_faults(faults), encode=True)
+    torch.cuda.synchronize()
+    O_faulty = host(O)
+    lay.verify_correct_sums(Dd, Wd, O, coc=True)
+    rep = lay.read_report()
+    b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
+    cd1, cd2 = wf.encode(D, 0)
+    np.testing.assert_allclose(b["cd1"], cd1.ravel(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(b["cd2"], cd2.ravel(), rtol=1e-12, atol=1e-10)
+    ck = wf.Checksums(cd1, cd2, *wf.encode(W, 0))
+    wf.coc_checksums(ck, spec.stride, spec.pad)
+    for name, ref in [("co5", ck.co5), ("co6", ck.co6), ("co7", ck.co7)]:
+        assert_close_scaled(b[name].reshape(ref.shape), ref, 1e-11, name)
+    ores = wf.protect(D, W, spec.stride, spec.pad, spec.dtype, O_in=O_faulty).report
+    assert rep.detected and ores.detected
+    assert rep.n_flagged == ores.n_flagged == 2
+    assert rep.fixes == ores.fixes
+    assert sorted(f[:4] for f in rep.fixes) == sorted((f.n, f.m, f.x, f.y) for f in faults)
+    assert rep.status == ft.STATUS_CORRECTED
+
+
+def test_verify_taps_when_conv_launch_left_no_partials():
+    """A channels-last layer whose convolution launch was given Cd but not Cw computes Co5..Co7
+    from the taps in the final launch instead: same checksums and verdict."""
+    spec = _split_spec((64, 32, 9, 40, 3, 1, 1, "f32"))
+    D, W = wl.gen_int_d(spec, 5), wl.gen_int_w(spec, 5)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, "f32"), dev(W, "f32")
+    lay.encode_weights(Wd)
+    O = lay.empty_output()
+    ck = ft._lib.Checksums()
+    ck.cd1, ck.cd2 = lay.buf["cd1"].data_ptr(), lay.buf["cd2"].data_ptr()
+    ft.conv_fwd_sums(lay.desc, Dd, Wd, O, ck, lay.report, lay.cap, lay.workspace)
+    lay.verify_correct_sums(Dd, Wd, O, coc=True)
+    torch.cuda.synchronize()
+    b = {k: v.cpu().numpy() for k, v in lay.buf.items()}
+    cd1, cd2 = wf.encode(D, 0)
+    ckr = wf.Checksums(cd1, cd2, *wf.encode(W, 0))
+    wf.coc_checksums(ckr, spec.stride, spec.pad)
+    for name, ref in [("co5", ckr.co5), ("co6", ckr.co6), ("co7", ckr.co7)]:
+        np.testing.assert_array_equal(b[name].reshape(ref.shape), ref)
+        np.testing.assert_array_equal(b[name], b["so" + name[2]])
+    assert not lay.read_report().detected
