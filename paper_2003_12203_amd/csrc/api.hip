@@ -102,19 +102,23 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     pl->off_sums = off;
     off += align256(4ull * pl->sum_splits * EF * sizeof(double));
     // channels-last copies of D and W for the vector-gather convolution; the copy of D encodes
-    // Cd1, Cd2 too, over image ranges when the layer has few 32 x 32 tiles.  A range keeps at least
-    // 64 bytes of D per element of its float64 partial pair (16 images in fp32, 32 in bf16), so the
-    // partials cost at most a quarter of D's traffic
+    // Cd1, Cd2 too, over image ranges when the layer has few tiles: enough ranges for about 1024
+    // workgroups, with at least 16 images (fp32) or 32 (bf16) a range, so that the float64 partial
+    // pairs (16 bytes per element of Cd) cost at most a quarter of D's traffic, and at most 16
     pl->nhwc = nhwc_layer(g);
     const size_t es = g.dtype == FTCNN_F32 ? 4 : 2;
     pl->prep_ns = 1;
     pl->co_in_conv = false;
     pl->co = CocTile{1, 1, 1, 1, 1, 1, 0, 1};
     if (pl->nhwc) {
-        const long long tiles = (long long)(g.C / 32) * ceil_div((long long)g.H * g.W, 32);
-        const int min_imgs = g.dtype == FTCNN_F32 ? 16 : 32;
-        pl->prep_ns = clampi(ceil_div(1024, tiles), 1, g.N / min_imgs > 1 ? g.N / min_imgs : 1);
-        // Co5..Co7 in extra workgroups of the convolution launch, in its threads and LDS
+        const long long tiles = (long long)(g.C / prep_tile_channels(g)) * ceil_div((long long)g.H * g.W, prep_tile_positions(g));
+        const int min_imgs = g.dtype == FTCNN_F32 ? 16 : 32;   // a multiple of both image batches
+        long long most = g.N / min_imgs;
+        most = most > 16 ? 16 : (most < 1 ? 1 : most);
+        pl->prep_ns = clampi(ceil_div(1024, tiles), 1, most);
+        // Co5..Co7 in extra workgroups of the convolution launch, in its threads and LDS, for
+        // layers with many taps to evaluate (E*F*K of at least 1M) and unsplit input checksums;
+        // on the others the final launch evaluates the taps itself in a few microseconds
         int nt = 0;
         size_t lds = 0;
         conv_tile_shape(g, &nt, &lds);
@@ -123,7 +127,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
         co.ty = nt / co.tx < g.E ? nt / co.tx : g.E;
         auto window = [&](int ty) { return (size_t)((ty - 1) * g.U + g.R) * ((co.tx - 1) * g.U + g.S); };
         while (co.ty > 1 && 2 * sizeof(double) * window(co.ty) > lds) co.ty /= 2;
-        if (2 * sizeof(double) * window(co.ty) <= lds) {
+        if (pl->prep_ns == 1 && EF * K >= (1LL << 20) && 2 * sizeof(double) * window(co.ty) <= lds) {
             pl->co_in_conv = true;
             const size_t cc = lds / (2 * sizeof(double) * window(co.ty));
             co.cc = (int)(cc < 8 ? cc : 8);
@@ -141,7 +145,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     pl->off_encp = off;
     off += pl->prep_ns > 1 ? align256(2ull * pl->prep_ns * CHW * sizeof(double)) : 0;
     pl->off_copart = off;
-    off += pl->co_in_conv ? align256(3ull * pl->co.groups * EF * sizeof(double)) : 0;
+    off += pl->co_in_conv ? align256(3ull * pl->co.groups * pl->prep_ns * EF * sizeof(double)) : 0;
     pl->off_corr = off;
     off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
     pl->bytes = off;

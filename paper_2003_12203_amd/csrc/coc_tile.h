@@ -6,10 +6,13 @@
 //             split order (only when the images were split);
 //   CoC       the checksum-of-checksum products of Sec. 3.2 at every output
 //             position, Co5 = Cd1 (x) Cw1, Co6 = Cd1 (x) Cw2, Co7 = Cd2 (x) Cw1,
-//             as partial products over ranges of input channels; the final
-//             detection launch adds the ranges in order.
+//             as partial products over ranges of input channels and, when the
+//             images were split, over the image ranges (the products are linear
+//             in Cd1 and Cd2, so each image range's partial checksums give their
+//             share); the final detection launch adds the slices in order.
 //
-// A CoC workgroup owns a tile of output positions and one channel range.  For
+// A CoC workgroup owns a tile of output positions, one channel range and one
+// image range (or the combined Cd when the images were not split).  For
 // each group of cc channels it stages the tile's input window of Cd1 and Cd2
 // (float64, zero outside the feature map) in LDS, then every thread evaluates
 // the R x S taps of its own position from there: each checksum element is read
@@ -50,15 +53,17 @@ __device__ inline void combine_block(const Geom &g, const CdSrc &src, double *__
     }
 }
 
-// One CoC workgroup (blk < tiles * groups), using lds (2 * cc * window doubles).
-// Writes slice `group` of copart [groups][3][E*F]: this channel range's share
-// of Co5, Co6, Co7 at the tile's positions.  Each thread sums its taps in the
-// fixed order (channel, r, s).
+// One CoC workgroup (blk < tiles * groups * ns), using lds (2 * cc * window
+// doubles).  Writes slice (group * ns + split) of copart [groups * ns][3][E*F]:
+// the share of Co5, Co6, Co7 at the tile's positions of one channel range and
+// one image range.  Each thread sums its taps in the fixed order (channel, r, s).
 template <int NT>
 __device__ inline void coc_block(const Geom &g, const CocTile &ct, const CdSrc &src, const double *__restrict__ cw1,
                                  const double *__restrict__ cw2, double *__restrict__ copart, int blk,
                                  double *lds) {
-    const int tile = blk % ct.tiles, grp = blk / ct.tiles;
+    const int tile = blk % ct.tiles, gs = blk / ct.tiles;
+    const int grp = gs / src.ns, split = gs - grp * src.ns;
+    const double *p1 = src.p1 + (long long)split * src.stride, *p2 = src.p2 + (long long)split * src.stride;
     const int bx = tile / ct.tiles_x, by = tile - (tile / ct.tiles_x) * ct.tiles_x;
     const int x0 = bx * ct.ty, y0 = by * ct.tx;
     const int rows = ct.ty < g.E - x0 ? ct.ty : g.E - x0;
@@ -83,8 +88,8 @@ __device__ inline void coc_block(const Geom &g, const CocTile &ct, const CdSrc &
             double a1 = 0.0, a2 = 0.0;
             if ((unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W) {
                 const long long idx = ((long long)(cb + c) * g.H + ih) * g.W + iw;
-                a1 = cd_at(src.p1, src.stride, src.ns, idx);
-                a2 = cd_at(src.p2, src.stride, src.ns, idx);
+                a1 = p1[idx];
+                a2 = p2[idx];
             }
             s1[e] = a1;
             s2[e] = a2;
@@ -108,7 +113,7 @@ __device__ inline void coc_block(const Geom &g, const CocTile &ct, const CdSrc &
     }
     if (mine) {
         const int p = (x0 + tyi) * g.F + y0 + txi;
-        double *o = copart + (size_t)grp * 3 * g.EF + p;
+        double *o = copart + (size_t)gs * 3 * g.EF + p;
         o[0] = c5;
         o[g.EF] = c6;
         o[2 * (size_t)g.EF] = c7;

@@ -877,9 +877,9 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
             }
             const bool coc = pl.co_in_conv && ck->cw1 && ck->cw2;
             const int comb = ns > 1 ? pl.co.comb_blocks : 0;
-            aux_blocks = comb + (coc ? pl.co.tiles * pl.co.groups : 0);
+            aux_blocks = comb + (coc ? pl.co.tiles * pl.co.groups * ns : 0);
             aux_kind = aux_blocks > 0 ? 2 : 0;
-            co_slices = coc ? pl.co.groups : 0;
+            co_slices = coc ? pl.co.groups * ns : 0;
         }
     } else if (cd1) {
         aux_kind = 1;   // encode workgroups; their count follows the tile's threads

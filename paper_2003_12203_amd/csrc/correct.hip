@@ -847,10 +847,10 @@ hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, cons
     double *scratch = reinterpret_cast<double *>(w + pl.off_corr);
     // Co5..Co7 of a channels-last layer come as partial slices from the convolution launch
     // (the kernel checks rep->reserved[1] and falls back to the taps)
-    const int taps = coc ? (pl.co_in_conv ? pl.co.groups : pl.g.K) : 0;
+    const int taps = coc ? (pl.co_in_conv ? pl.co.groups * pl.prep_ns : pl.g.K) : 0;
     const int tpp = final_tpp(sp, taps, pl.g.EF);
     const double *copart = reinterpret_cast<const double *>(w + pl.off_copart);
-    const int max_groups = pl.co_in_conv ? pl.co.groups : 0;
+    const int max_groups = pl.co_in_conv ? pl.co.groups * pl.prep_ns : 0;
     const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
 #define VC(TPP, COC)                                                                                            \
     verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, copart, max_groups, ck.co5,       \

@@ -26,8 +26,9 @@ struct Geom {
 // Tiling of the Co5..Co7 products computed by extra workgroups of the
 // convolution launch (channels-last layers): output tiles of tx columns (of F)
 // by ty rows (of E), cc channels staged in LDS per step, the channels split
-// into `groups` ranges; comb_blocks workgroups combine the image-split
-// partials of Cd1, Cd2 when ns > 1.
+// into `groups` ranges and, when the input checksums come as ns image-range
+// partials, one workgroup per range as well (groups * ns partial slices);
+// comb_blocks workgroups combine those partials into Cd1, Cd2.
 struct CocTile {
     int tx, ty, cc;
     int tiles_x, tiles;
@@ -145,8 +146,17 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
 int conv_tile_m(const Geom &g);
 // Threads per workgroup and dynamic LDS bytes of the convolution chosen for this layer.
 void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes);
-// Layers whose convolution reads channels-last copies (pl.nhwc): Ch a multiple of 32.
-inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0; }
+// Layers whose convolution reads channels-last copies (pl.nhwc): Ch a multiple of 32 (and
+// kernels of at most 4096 taps, whose weight rows the copy stages in LDS).
+inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0 && g.R * g.S <= 4096; }
+// Positions per tile of the channels-last copy (128 bytes of one channel) and channels per
+// tile (64 for bf16 when that still leaves 512 tiles: a stored position is then one 128-byte
+// line).
+inline int prep_tile_positions(const Geom &g) { return g.dtype == FTCNN_F32 ? 32 : 64; }
+inline int prep_tile_channels(const Geom &g) {
+    const long long hw_tiles = ((long long)g.H * g.W + prep_tile_positions(g) - 1) / prep_tile_positions(g);
+    return g.dtype == FTCNN_BF16 && g.C % 64 == 0 && (g.C / 64) * hw_tiles >= 512 ? 64 : 32;
+}
 // Dt = D in [n][h][w][c] order and Wt = W in [m][r][s][c] order into the workspace
 // (pl.off_dt, pl.off_wt); with cd1 and cd2 set, the copy of D also encodes them
 // (directly when pl.prep_ns == 1, else as image-split partials at pl.off_encp
