@@ -262,6 +262,16 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
                          ftcnn_report *rep, int32_t cap_fixes, void *workspace,
                          hipStream_t stream);
 
+/* INSTRUMENTATION (measurement, not an operation of the paper): the next call
+ * on the calling thread that launches the convolution kernel (ftcnn_conv_fwd,
+ * ftcnn_conv_fwd_ws, ftcnn_conv_fwd_sums, ftcnn_protected_conv) records
+ * `before` on its stream immediately before that launch and `after`
+ * immediately after it, so that their elapsed time is the kernel's alone (the
+ * channels-last copy and the other launches of the call fall outside); the
+ * hook is then cleared.  Either may be NULL.  The events must be created by
+ * the caller (with timing enabled) on the device of that stream. */
+int ftcnn_set_kernel_events(hipEvent_t before, hipEvent_t after);
+
 /* TEST ONLY: corrupt stored outputs, reproducing the paper's source-level
  * fault injection (Sec. 6.1).  faults is a HOST array of at most 64 entries
  * (ftcnn_fault above), applied in order.  Positions must be in range. */

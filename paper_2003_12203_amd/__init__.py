@@ -139,6 +139,21 @@ def protected_conv(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
                                       _stream(stream)), "ftcnn_protected_conv")
 
 
+def set_kernel_events(before, after) -> None:
+    """ftcnn_set_kernel_events: record two torch.cuda.Event objects (timing enabled) around the next
+    launch of the convolution kernel on this thread.  The events are recorded once here first so
+    that their HIP handles exist."""
+    handles = []
+    for ev in (before, after):
+        if ev is None:
+            handles.append(None)
+            continue
+        if ev.cuda_event == 0:
+            ev.record()
+        handles.append(C.c_void_p(ev.cuda_event))
+    _check(lib().ftcnn_set_kernel_events(*handles), "ftcnn_set_kernel_events")
+
+
 def _fault_array(faults: Sequence[dict]):
     arr = (_lib.Fault * max(1, len(faults)))()
     kinds = {"flip": 0, "add": 1, "set": 2}

@@ -56,7 +56,7 @@ class Fault(C.Structure):
 EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ftcnn_last_error",
            "ftcnn_encode", "ftcnn_conv_fwd", "ftcnn_checksum_conv", "ftcnn_verify", "ftcnn_correct",
            "ftcnn_verify_correct", "ftcnn_conv_fwd_ws", "ftcnn_conv_fwd_sums", "ftcnn_verify_correct_sums", "ftcnn_protected_conv",
-           "ftcnn_inject")
+           "ftcnn_inject", "ftcnn_set_kernel_events")
 
 _lib = None
 
@@ -105,5 +105,7 @@ def load(path: str = LIB_PATH):
     L.ftcnn_protected_conv.restype = C.c_int
     L.ftcnn_inject.argtypes = [P(ConvDesc), _dp, P(Fault), C.c_int32, _dp]
     L.ftcnn_inject.restype = C.c_int
+    L.ftcnn_set_kernel_events.argtypes = [_dp, _dp]
+    L.ftcnn_set_kernel_events.restype = C.c_int
     _lib = L
     return L

@@ -10,6 +10,7 @@ namespace ftcnn {
 namespace {
 
 thread_local char g_err[512] = "";
+thread_local KernelEvents g_events{nullptr, nullptr};
 
 int fail(int code, const char *fmt, ...) {
     va_list ap;
@@ -299,6 +300,9 @@ int do_correct(const Plan &pl, const void *D, const void *W, void *O, const ftcn
 }
 
 }  // namespace
+
+KernelEvents &kernel_events() { return g_events; }
+
 }  // namespace ftcnn
 
 using namespace ftcnn;
@@ -306,6 +310,12 @@ using namespace ftcnn;
 extern "C" {
 
 const char *ftcnn_last_error(void) { return g_err; }
+
+int ftcnn_set_kernel_events(hipEvent_t before, hipEvent_t after) {
+    g_events.before = before;
+    g_events.after = after;
+    return FTCNN_OK;
+}
 
 int ftcnn_out_shape(const ftcnn_conv_desc *desc, int32_t *E, int32_t *F) {
     Plan pl;

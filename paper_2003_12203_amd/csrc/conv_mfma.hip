@@ -775,10 +775,22 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
         if (attr != hipSuccess) return attr;
     }
+    KernelEvents &ev = kernel_events();
+    if (ev.before) {
+        const hipError_t r = hipEventRecord(ev.before, st);
+        if (r != hipSuccess) return r;
+    }
     kern<<<(unsigned)grid, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D),
                                                                static_cast<const T *>(W), static_cast<T *>(O), g,
                                                                tiles_m, (int)total, m_major, e);
-    return hipGetLastError();
+    const hipError_t r = hipGetLastError();
+    if (r != hipSuccess) return r;
+    if (ev.after) {
+        const hipError_t r2 = hipEventRecord(ev.after, st);
+        if (r2 != hipSuccess) return r2;
+    }
+    ev.before = ev.after = nullptr;
+    return hipSuccess;
 }
 
 // One tile configuration, dispatched on the weight alignment and the epilogue.

@@ -124,6 +124,15 @@ __device__ inline bool is_bad(double d, double q, double scale) {
     return !isfinite(d) || fabs(d) > scale * q;
 }
 
+// ---- instrumentation ------------------------------------------------------
+
+// Events the caller asked to have recorded around the next launch of the
+// convolution kernel on this thread (ftcnn_set_kernel_events); cleared once used.
+struct KernelEvents {
+    hipEvent_t before, after;
+};
+KernelEvents &kernel_events();
+
 // ---- launches (one per kernel family; defined in the .hip files) ----------
 
 hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, double *c2,
