@@ -28,6 +28,11 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
+// A 16-byte unit, or zeros: the selects work on whole 32-bit words.
+__device__ inline uint4 keep_or_zero(bool ok, uint4 v) {
+    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+}
+
 // Map the hardware workgroup id onto a logical tile so that each XCD (ids are
 // dealt round-robin over 8 XCDs) receives a contiguous run of logical tiles.
 __device__ inline int xcd_tile(int bid, int total) {
@@ -115,7 +120,8 @@ __device__ inline typename C::Mask load_a(const typename C::T *__restrict__ Wt, 
             // through a uint4 pointer so the load is one global_load_dwordx4
             const bool ok = (as.base[i] >= 0) & (k < g.K);
             const uint4 *w4 = reinterpret_cast<const uint4 *>(Wt);
-            ra[i].q = w4[ok ? (as.base[i] + kbase) / C::VEC : 0];
+            // an invalid slot (k >= K or a row past M) reads element 0 and keeps zeros
+            ra[i].q = keep_or_zero(ok, w4[ok ? (as.base[i] + kbase) / C::VEC : 0]);
             mask |= (ok ? ((M(1) << C::VEC) - M(1)) : M(0)) << (i * C::VEC);
         } else {
 #pragma unroll
@@ -171,7 +177,9 @@ __device__ inline typename C::Mask load_b(const typename C::T *__restrict__ Dt, 
     return mask;
 }
 
-template <typename C>
+// NOMASK: the gathers zeroed every invalid element already (channels-last layers
+// with 16-byte weight rows), so the registers go to LDS as they are.
+template <typename C, bool NOMASK = false>
 __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
                                  Pack<typename C::T, C::VEC> (&ra)[C::A_PER], typename C::Mask amask,
                                  Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC], typename C::Mask bmask,
@@ -181,17 +189,21 @@ __device__ inline void store_lds(typename C::T *As, typename C::T *Bs, int tid,
     for (int i = 0; i < C::A_PER; ++i) {
         const int slot = tid + i * C::NT;
         if (C::A_SLOTS % C::NT == 0 || slot < C::A_SLOTS) {
+            if constexpr (!NOMASK) {
 #pragma unroll
-            for (int v = 0; v < C::VEC; ++v)
-                ra[i].e[v] = ((amask >> (i * C::VEC + v)) & 1) ? ra[i].e[v] : T(0);
+                for (int v = 0; v < C::VEC; ++v)
+                    ra[i].e[v] = ((amask >> (i * C::VEC + v)) & 1) ? ra[i].e[v] : T(0);
+            }
             const int row = slot / (C::TK / C::VEC);
             const int kq = slot % (C::TK / C::VEC);
             *reinterpret_cast<uint4 *>(&As[row * C::LDK + kq * C::VEC]) = ra[i].q;
         }
     }
+    if constexpr (!NOMASK) {
 #pragma unroll
-    for (int j = 0; j < C::KR; ++j)
-        rb[j / C::VEC].e[j % C::VEC] = ((bmask >> j) & 1) ? rb[j / C::VEC].e[j % C::VEC] : T(0);
+        for (int j = 0; j < C::KR; ++j)
+            rb[j / C::VEC].e[j % C::VEC] = ((bmask >> j) & 1) ? rb[j / C::VEC].e[j % C::VEC] : T(0);
+    }
 #pragma unroll
     for (int j = 0; j < C::KR; j += C::VEC)
         *reinterpret_cast<uint4 *>(&Bs[bp * C::LDK + bkg * C::KR + j]) = rb[j / C::VEC].q;
@@ -273,10 +285,10 @@ __device__ inline typename C::Mask load_b_nhwc(const typename C::T *__restrict__
     const int r = rs / g.S, s = rs - r * g.S;
     const int ih = ih0 + r, iw = iw0 + s;
     const bool ok = pvalid & (kstart < g.K) & ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
-    const int base = ok ? img_base + (ih * g.W + iw) * g.C + c0 : 0;   // a multiple of KR: 16-byte aligned
-    const uint4 *src = reinterpret_cast<const uint4 *>(Dt + base);
+    // a multiple of KR: 16-byte aligned; a run outside the image reads element 0 and keeps zeros
+    const uint4 *src = reinterpret_cast<const uint4 *>(Dt + (ok ? img_base + (ih * g.W + iw) * g.C + c0 : 0));
 #pragma unroll
-    for (int i = 0; i < C::KR / C::VEC; ++i) rb[i].q = src[i];
+    for (int i = 0; i < C::KR / C::VEC; ++i) rb[i].q = keep_or_zero(ok, src[i]);
     using M = typename C::Mask;
     constexpr M all = C::KR == 8 * (int)sizeof(M) ? ~M(0) : ((M(1) << C::KR) - M(1));
     return ok ? all : 0u;
@@ -484,7 +496,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     typename C::Mask amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
     typename C::Mask bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
                           : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
-    store_lds<C>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
+    store_lds<C, NHWC>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
     __syncthreads();
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
@@ -506,12 +518,12 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             amask = load_a<C>(Wt, g, (kc + 2) * C::TK, KVEC, as, ra);
             bmask = load_b_nhwc<C>(D, g, (kc + 2) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
             mma_chunk<C, FM, FP>(A0, B0, lane, arow0, brow0, acc);
-            store_lds<C>(A1, B1, tid, ra2, amask2, rb2, bmask2, bp, bkg);
+            store_lds<C, NHWC>(A1, B1, tid, ra2, amask2, rb2, bmask2, bp, bkg);
             __syncthreads();
             amask2 = load_a<C>(Wt, g, (kc + 3) * C::TK, KVEC, as, ra2);
             bmask2 = load_b_nhwc<C>(D, g, (kc + 3) * C::TK + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb2);
             mma_chunk<C, FM, FP>(A1, B1, lane, arow0, brow0, acc);
-            store_lds<C>(A0, B0, tid, ra, amask, rb, bmask, bp, bkg);
+            store_lds<C, NHWC>(A0, B0, tid, ra, amask, rb, bmask, bp, bkg);
             __syncthreads();
         }
         if (kc < nchunks) mma_chunk<C, FM, FP>(A0, B0, lane, arow0, brow0, acc);   // odd count: the last chunk
@@ -524,7 +536,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             amask = load_a<C>(Wt, g, kb, KVEC, as, ra);
             bmask = load_b_nhwc<C>(D, g, kb + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
             mma_chunk<C, FM, FP>(As0 + buf * C::TM * C::LDK, Bs0 + buf * C::TP * C::LDK, lane, arow0, brow0, acc);
-            store_lds<C>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
+            store_lds<C, NHWC>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
                          bmask, bp, bkg);
             __syncthreads();
         }
