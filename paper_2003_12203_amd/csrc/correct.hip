@@ -89,6 +89,11 @@ template <> __device__ inline void put_bits<uint16_t>(uint16_t *p, long long i, 
 template <typename T> __device__ inline void store_val(T *p, long long i, double v) {
     Elem<T>::store(p, i, (float)v);
 }
+// The value store_val leaves in memory, widened back to float64.
+template <typename T> __device__ inline double stored_value(double v) {
+    if constexpr (sizeof(T) == 4) return (double)(float)v;
+    else return (double)bf16_bits_to_f32(f32_to_bf16_bits((float)v));
+}
 
 template <typename T> __device__ inline long long oidx(const Ctx<T> &c, int n, int m, int p) {
     return ((long long)n * c.g.M + m) * c.g.EF + p;
@@ -379,6 +384,22 @@ __device__ bool scheme_coc(const Ctx<T> &c, Sh &sh, int p, int x, int y, const d
     const int i = legal(ri, c.g.N, c.eta), j = legal(rj, c.g.M, c.eta);
     if (i < 0 || j < 0) return false;
     begin_scheme<T>(sh);
+    // one pass over the other blocks at p: their sums give the repair (the exclusive sum of R7)
+    // and, with the repaired value added, the re-summed checksums of the consistency check
+    const double wb = (double)c.wb;
+    double e[6] = {0, 0, 0, 0, 0, 0};
+    for_blocks(c, p, [&](int n, int m, double o) {
+        if (n != i || m != j) {
+            const double t6 = ((double)m + wb) * o, t7 = ((double)n + wb) * o;
+            e[0] += o;
+            e[1] += t6;
+            e[2] += t7;
+            e[3] = fma(o, o, e[3]);
+            e[4] = fma(t6, t6, e[4]);
+            e[5] = fma(t7, t7, e[5]);
+        }
+    });
+    bsum<6>(e, sh);
     double v;
     if (c.recompute) {
         double a[1] = {0.0};
@@ -394,15 +415,19 @@ __device__ bool scheme_coc(const Ctx<T> &c, Sh &sh, int p, int x, int y, const d
         bsum<1>(a, sh);
         v = a[0];
     } else {
-        double a[1] = {0.0};
-        for_blocks(c, p, [&](int n, int m, double o) {
-            if (n != i || m != j) a[0] += o;
-        });
-        bsum<1>(a, sh);
-        v = co[0] - a[0];
+        v = co[0] - e[0];
     }
     if (threadIdx.x == 0) repair(c, sh, i, j, p, v);
-    return settle(c, sh, p, co);
+    __syncthreads();
+    // the value as stored, and the checksums of the position re-summed with it
+    const double o = stored_value<T>(v);
+    const double t6 = ((double)j + wb) * o, t7 = ((double)i + wb) * o;
+    const double s0 = e[0] + o, s1 = e[1] + t6, s2 = e[2] + t7;
+    const double q5 = sqrt(fma(o, o, e[3])), q6 = sqrt(fma(t6, t6, e[4])), q7 = sqrt(fma(t7, t7, e[5]));
+    if (!is_bad(co[0] - s0, q5, c.scale) && !is_bad(co[1] - s1, q6, c.scale) && !is_bad(co[2] - s2, q7, c.scale))
+        return true;
+    undo(c, sh, p);
+    return false;
 }
 
 template <typename T>
