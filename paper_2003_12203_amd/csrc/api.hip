@@ -143,6 +143,8 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     off += pl->nhwc ? align256((size_t)g.N * CHW * es) : 0;
     pl->off_wt = off;
     off += pl->nhwc ? align256((size_t)g.M * K * es) : 0;
+    pl->off_zero = off;   // 256 zero bytes for loads that fall outside the operands (written by the copy)
+    off += pl->nhwc ? 256 : 0;
     pl->off_encp = off;
     off += pl->prep_ns > 1 ? align256(2ull * pl->prep_ns * CHW * sizeof(double)) : 0;
     pl->off_copart = off;

@@ -374,6 +374,140 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
     }
 }
 
+// ---- direct-to-LDS main loop (bf16, channels-last, 64-deep chunks) ----------
+//
+// global_load_lds_dwordx4 moves 16 bytes per lane from global memory straight
+// into LDS: lane L of a wave lands at the instruction's LDS base + 16*L (the
+// base is wave-uniform), while every lane picks its own global address.  The
+// tiles are kept as rows of 64 bf16 (128 bytes, eight 16-byte chunks) with
+// chunk c of row r stored at position c ^ (r & 7), so one instruction fills
+// eight whole rows and the matrix-core reads of 32 consecutive rows spread
+// over all banks.  Two LDS stages: chunk k + 2 is requested into the stage of
+// chunk k as soon as every wave has read chunk k, so a chunk's loads have a
+// whole chunk of MFMAs to land.  Waits on the loads are explicit (vmcnt), and
+// the barriers carry compiler-only fences: a memory fence would make the
+// compiler wait for every load in flight, the next chunk's included.
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void glb_cvoid_t;
+
+// s_waitcnt: at most V vector-memory operations of this wave outstanding.
+template <int V> __device__ inline void wait_vmcnt() {
+    static_assert(V >= 0 && V < 64, "vmcnt is six bits");
+    __builtin_amdgcn_s_waitcnt((V & 15) | (0x7 << 4) | (0xF << 8) | ((V >> 4) << 14));
+}
+// s_waitcnt: no LDS operation of this wave outstanding.
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+// Workgroup barrier that orders LDS accesses around it in the compiler only.
+__device__ inline void lds_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// One chunk of MFMAs from a swizzled stage.  The fragments of k-step q + 1 are
+// read while the MFMAs of step q run (sched_barrier keeps the two groups
+// apart), so no MFMA waits on the read right before it.
+template <typename C, int FM, int FP>
+__device__ inline void mma_chunk_swz(const unsigned char *As, const unsigned char *Bs, int lane, int arow0, int brow0,
+                                     floatx16 (&acc)[FM][FP]) {
+    const int l32 = lane & 31, h = lane >> 5, sw = l32 & 7;
+    const unsigned char *arow = As + (arow0 + l32) * 128, *brow = Bs + (brow0 + l32) * 128;
+    bf16x8 a[2][FM], b[2][FP];
+    auto load = [&](int q, int slot) {
+        const int pos = ((4 * h + q) ^ sw) * 16;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+            a[slot][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(arow + i * 32 * 128 + pos));
+#pragma unroll
+        for (int j = 0; j < FP; ++j)
+            b[slot][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(brow + j * 32 * 128 + pos));
+    };
+    load(0, 0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (q + 1 < 4) load(q + 1, (q + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FP; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q & 1][i], b[q & 1][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// The whole K loop of one tile.  zp: 16 zero bytes that lanes whose row or tap
+// lies outside the operands load instead.  Needs Ch % 64 == 0 (a chunk is one
+// (r, s) tap of 64 channels) and 2 * (TM + TP) * 128 bytes of LDS.
+template <typename C, int FM, int FP>
+__device__ inline void dma_mainloop(const uint16_t *__restrict__ Dt, const uint16_t *__restrict__ Wt, const Geom &g,
+                                    int m0, long long p0, const uint16_t *zp, unsigned char *smem,
+                                    floatx16 (&acc)[FM][FP], int tid, int arow0, int brow0) {
+    constexpr int NW = C::NT / 64;
+    constexpr int NIA = C::TM / (8 * NW), NIB = C::TP / (8 * NW), NI = NIA + NIB;
+    static_assert(C::TM % (8 * NW) == 0 && C::TP % (8 * NW) == 0 && NI < 64, "DMA tile shape");
+    constexpr int STAGE_A = C::TM * 128, STAGE = (C::TM + C::TP) * 128;
+    const int lane = tid & 63, w = tid >> 6;
+    const int lr = lane >> 3;              // row of the instruction's eight
+    const int cg = (lane & 7) ^ lr;        // global chunk this lane loads (its LDS chunk is lane & 7)
+    int a_off[NIA];
+    bool a_ok[NIA];
+#pragma unroll
+    for (int j = 0; j < NIA; ++j) {
+        const int m = m0 + (j * NW + w) * 8 + lr;
+        a_ok[j] = m < g.M;
+        a_off[j] = (a_ok[j] ? m : 0) * g.K + cg * 8;
+    }
+    int b_base[NIB], b_ih[NIB], b_iw[NIB];
+    bool b_ok[NIB];
+#pragma unroll
+    for (int j = 0; j < NIB; ++j) {
+        const long long pg = p0 + (j * NW + w) * 8 + lr;
+        b_ok[j] = pg < g.P_total;
+        const int n = b_ok[j] ? (int)(pg / g.EF) : 0;
+        const int pix = b_ok[j] ? (int)(pg - (long long)n * g.EF) : 0;
+        const int x = pix / g.F, y = pix - (pix / g.F) * g.F;
+        b_ih[j] = g.U * x - g.P;
+        b_iw[j] = g.U * y - g.P;
+        b_base[j] = n * (int)g.CHW + cg * 8;
+    }
+    const uintptr_t zpa = reinterpret_cast<uintptr_t>(zp);
+    auto issue = [&](int kc, int st) {
+        const int kb = kc * 64;
+        const int rs = kb / g.C, c0 = kb - rs * g.C;
+        const int r = rs / g.S, s = rs - (rs / g.S) * g.S;
+        unsigned char *base = smem + st * STAGE;
+#pragma unroll
+        for (int j = 0; j < NIA; ++j) {
+            // the address is selected as an integer: a pointer select would become a branch
+            const uintptr_t src = a_ok[j] ? reinterpret_cast<uintptr_t>(Wt + a_off[j] + kb) : zpa;
+            __builtin_amdgcn_global_load_lds((glb_cvoid_t *)src, (lds_void_t *)(base + (j * NW + w) * 8 * 128), 16, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            const int ih = b_ih[j] + r, iw = b_iw[j] + s;
+            const bool ok = b_ok[j] & ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
+            const uintptr_t src = ok ? reinterpret_cast<uintptr_t>(Dt + b_base[j] + (ih * g.W + iw) * g.C + c0) : zpa;
+            __builtin_amdgcn_global_load_lds((glb_cvoid_t *)src,
+                                             (lds_void_t *)(base + STAGE_A + (j * NW + w) * 8 * 128), 16, 0, 0);
+        }
+    };
+    const int nch = g.K / 64;
+    issue(0, 0);
+    if (nch > 1) issue(1, 1);
+    for (int kc = 0; kc < nch; ++kc) {
+        if (kc + 1 < nch) wait_vmcnt<NI>();   // this wave's loads of chunk kc have landed
+        else wait_vmcnt<0>();
+        lds_barrier();                        // ... and every wave's
+        const unsigned char *st = smem + (kc & 1) * STAGE;
+        mma_chunk_swz<C, FM, FP>(st, st + STAGE_A, lane, arow0, brow0, acc);
+        wait_lgkm0();
+        lds_barrier();                        // every wave has read the stage
+        if (kc + 2 < nch) issue(kc + 2, kc & 1);
+    }
+}
+
 // Epilogue arguments.  EPI 0: plain store.  EPI 1: the CoC-D summations of
 // every stored value as well (Sec. 3.6): for each pixel p of the tile, the tile's
 // rows give sum O, sum (m + wbase) O, (n + wbase) sum O and sum O^2, written as
@@ -420,7 +554,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
                                                             int tiles_m, int tiles_total, int m_major,
-                                                            Epi<EPI> ep) {
+                                                            const void *zp, Epi<EPI> ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
     using T = typename C::T;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -490,17 +624,24 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
+    const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
+    constexpr bool DMA = NHWC && WEAVE == 3 && sizeof(T) == 2 && C::TK == 64;
     Pack<T, C::VEC> ra[C::A_PER];
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
-    typename C::Mask amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
-    typename C::Mask bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
-                          : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
-    store_lds<C, NHWC>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
-    __syncthreads();
+    typename C::Mask amask = 0, bmask = 0;
+    if constexpr (!DMA) {
+        amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
+        bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
+                     : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+        store_lds<C, NHWC>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
+        __syncthreads();
+    }
 
-    const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    if constexpr (NHWC && WEAVE == 2) {
+    if constexpr (DMA) {
+        dma_mainloop<C, FM, FP>(reinterpret_cast<const uint16_t *>(D), reinterpret_cast<const uint16_t *>(Wt), g, m0,
+                                p0, static_cast<const uint16_t *>(zp), smem, acc, tid, arow0, brow0);
+    } else if constexpr (NHWC && WEAVE == 2) {
         // channels-last, two chunks in flight: chunk kc + 2 is loaded into one register set
         // while chunk kc is consumed from LDS, and chunk kc + 1 (loaded a whole chunk earlier,
         // in the other set) then goes to the other LDS buffer, so the stores wait only on loads
@@ -750,7 +891,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
 
 template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC>
 hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
-                      const Epi<EPI> &ep) {
+                      const void *zp, const Epi<EPI> &ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
     using T = typename C::T;
     static_assert(EPI == 0 || (size_t)WM * 3 * C::TP * sizeof(double) <= C::LDS_BYTES, "epilogue fold fits LDS");
@@ -794,7 +935,7 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     }
     kern<<<(unsigned)grid, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D),
                                                                static_cast<const T *>(W), static_cast<T *>(O), g,
-                                                               tiles_m, (int)total, m_major, e);
+                                                               tiles_m, (int)total, m_major, zp, e);
     const hipError_t r = hipGetLastError();
     if (r != hipSuccess) return r;
     if (ev.after) {
@@ -813,11 +954,17 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
     template <int EPI>
     static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep,
-                          bool nhwc = false) {
-        if (nhwc) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, ep);
-        const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
-        if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, false>(g, D, W, O, st, 0, ep);
-        return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI, false>(g, D, W, O, st, 0, ep);
+                          bool nhwc = false, const void *zp = nullptr) {
+        if constexpr (WEAVE == 3) {
+            // direct-to-LDS tiles exist for channels-last operands only
+            if (!nhwc || !zp) return hipErrorInvalidValue;
+            return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
+        } else {
+            if (nhwc) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
+            const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+            if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, false>(g, D, W, O, st, 0, zp, ep);
+            return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI, false>(g, D, W, O, st, 0, zp, ep);
+        }
     }
 };
 
@@ -825,9 +972,11 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
 // filter tile follows M so small-M layers waste no MFMA rows; for larger M the
 // biggest tile that still leaves about two workgroups per CU wins.  For bf16
 // (eight times the fp32 matrix rate per instruction) the channels-last loop
-// keeps two chunks in flight (WEAVE 2): 64 x 256 tiles for M <= 64, 256 x 256
-// tiles (a 128 x 128 block per wave) where there are enough of them, and
-// 128 x 128 tiles with 64-deep chunks elsewhere.
+// keeps two chunks in flight (WEAVE 2): 64 x 256 tiles for M <= 64, and for
+// 64-channel multiples direct-to-LDS loads (WEAVE 3): 256 x 256 tiles (a
+// 128 x 128 block per wave) for M >= 512 where there are enough of them,
+// 128 x 128 elsewhere; other layers take 256 x 256 or 128 x 128 tiles with
+// register-staged loads.
 long long n_tiles(const Geom &g, int tm, int tp) {
     return ((g.P_total + tp - 1) / tp) * (long long)((g.M + tm - 1) / tm);
 }
@@ -842,10 +991,13 @@ using BF16_M32 = Tile<BF16T<32>, 1, 4, 1, 2, 0>;
 using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, 2>;
 using BF16_128x128_K64 = Tile<BF16T<64>, 2, 2, 2, 2, 2>;
 using BF16_256x256 = Tile<BF16T<32>, 2, 2, 4, 4, 2>;
+using BF16_DMA_128x128 = Tile<BF16T<64>, 2, 2, 2, 2, 3>;
+using BF16_DMA_256x256 = Tile<BF16T<64>, 2, 2, 4, 4, 3>;
 
-// Calls f(TileType{}) for the tile this layer uses.
+// Calls f(TileType{}) for the tile this layer uses (nhwc: the launch reads the
+// channels-last copies).
 template <typename Fn>
-auto with_tile(const Geom &g, Fn &&f) {
+auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
     if (g.dtype == FTCNN_F32) {
         if (g.M <= 32) return f(F32_M32{});
         if (g.M <= 64) return f(F32_M64{});
@@ -856,6 +1008,11 @@ auto with_tile(const Geom &g, Fn &&f) {
     }
     if (g.M <= 32) return f(BF16_M32{});
     if (g.M <= 64) return f(BF16_M64{});
+    if (nhwc && g.C % 64 == 0) {
+        // direct-to-LDS loads: 256 x 256 where M is large and there are enough such tiles
+        if (g.M >= 512 && n_tiles(g, 256, 256) >= 192) return f(BF16_DMA_256x256{});
+        return f(BF16_DMA_128x128{});
+    }
     if (g.M >= 256 && n_tiles(g, 256, 256) >= 192) return f(BF16_256x256{});
     return f(BF16_128x128_K64{});
 }
@@ -863,16 +1020,16 @@ auto with_tile(const Geom &g, Fn &&f) {
 }  // namespace
 
 int conv_tile_m(const Geom &g) {
-    return with_tile(g, [](auto t) { return decltype(t)::TM; });
+    return with_tile(g, nhwc_layer(g), [](auto t) { return decltype(t)::TM; });
 }
 
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st) {
     const Epi<0> ep{};
-    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
+    return with_tile(pl.g, false, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
 void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes) {
-    with_tile(g, [&](auto t) {
+    with_tile(g, nhwc_layer(g), [&](auto t) {
         *threads = decltype(t)::NT;
         *lds_bytes = decltype(t)::LDS_BYTES;
         return 0;
@@ -885,6 +1042,7 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
     char *w = static_cast<char *>(ws);
     double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
     const void *Dc = D, *Wc = W;
+    const void *zp = pl.nhwc ? w + pl.off_zero : nullptr;   // zeroed by the channels-last copy
     int aux_kind = 0, aux_blocks = 0, co_slices = 0;
     CdSrc src{cd1, cd2, 0, 1};
     if (pl.nhwc) {
@@ -915,12 +1073,12 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
     const double *cw1 = ck ? ck->cw1 : nullptr, *cw2 = ck ? ck->cw2 : nullptr;
     if (nf == 0) {
         Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}};
-        return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc); });
+        return with_tile(pl.g, pl.nhwc, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp); });
     }
     Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
-    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc); });
+    return with_tile(pl.g, pl.nhwc, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp); });
 }
 
 hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st) {
@@ -929,7 +1087,9 @@ hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O,
     if (e != hipSuccess) return e;
     char *w = static_cast<char *>(ws);
     const Epi<0> ep{};
-    return with_tile(pl.g, [&](auto t) { return decltype(t)::run(pl.g, w + pl.off_dt, w + pl.off_wt, O, st, ep, true); });
+    return with_tile(pl.g, true, [&](auto t) {
+        return decltype(t)::run(pl.g, w + pl.off_dt, w + pl.off_wt, O, st, ep, true, w + pl.off_zero);
+    });
 }
 
 }  // namespace ftcnn

@@ -50,7 +50,7 @@ struct Plan {
     int prep_ns;                      // image ranges of the encode fused into the channels-last copy
     bool co_in_conv;                  // Co5..Co7 partials computed by workgroups of the convolution launch
     CocTile co;                       // their tiling (co_in_conv)
-    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, bytes;
+    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, off_zero, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
 

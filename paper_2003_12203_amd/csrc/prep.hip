@@ -45,7 +45,8 @@ template <typename T, bool ENC, int TC>
 __global__ __launch_bounds__(kThreads) void prep_kernel(const T *__restrict__ D, const T *__restrict__ W,
                                                         T *__restrict__ Dt, T *__restrict__ Wt, Geom g,
                                                         double *cd1, double *cd2, long long split_stride,
-                                                        int tr_blocks, int hw_tiles, int c_tiles, int ns, int vec_ok) {
+                                                        int tr_blocks, int hw_tiles, int c_tiles, int ns, int vec_ok,
+                                                        uint4 *__restrict__ zero16) {
     using P = PrepT<T, TC>;
     constexpr int VEC = P::VEC, TH = P::TH, LDT = P::LDT, RPT = P::RPT, BATCH = P::BATCH;
     __shared__ T tile[BATCH][TC][LDT];
@@ -151,6 +152,7 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(const T *__restrict__ D,
     // comes out as [R*S][C] (coalesced reads of W, runs of channels written to Wt)
     const int m = b - tr_blocks;
     if (m >= g.M) return;
+    if (m == 0 && threadIdx.x < 16) zero16[threadIdx.x] = make_uint4(0, 0, 0, 0);
     T *stage = &tile[0][0][0];
     const int RS = g.R * g.S;
     const int cch = P::LDS_ELEMS / RS < g.C ? (P::LDS_ELEMS / RS > 0 ? P::LDS_ELEMS / RS : 1) : g.C;
@@ -175,6 +177,7 @@ hipError_t run_tc(const Plan &pl, const void *D, const void *W, double *cd1, dou
     char *w = static_cast<char *>(ws);
     T *Dt = reinterpret_cast<T *>(w + pl.off_dt);
     T *Wt = reinterpret_cast<T *>(w + pl.off_wt);
+    uint4 *zero16 = reinterpret_cast<uint4 *>(w + pl.off_zero);
     const long long HW = (long long)g.H * g.W;
     const long long hw_tiles = (HW + P::TH - 1) / P::TH, c_tiles = g.C / TC;
     // without the encode every round of images is a workgroup of its own
@@ -195,12 +198,12 @@ hipError_t run_tc(const Plan &pl, const void *D, const void *W, double *cd1, dou
         prep_kernel<T, true, TC><<<(unsigned)grid, kThreads, 0, st>>>(static_cast<const T *>(D),
                                                                       static_cast<const T *>(W), Dt, Wt, g, o1, o2,
                                                                       stride, (int)tr, (int)hw_tiles, (int)c_tiles, ns,
-                                                                      vec_ok);
+                                                                      vec_ok, zero16);
     else
         prep_kernel<T, false, TC><<<(unsigned)grid, kThreads, 0, st>>>(static_cast<const T *>(D),
                                                                        static_cast<const T *>(W), Dt, Wt, g, nullptr,
                                                                        nullptr, 0, (int)tr, (int)hw_tiles,
-                                                                       (int)c_tiles, ns, vec_ok);
+                                                                       (int)c_tiles, ns, vec_ok, zero16);
     return hipGetLastError();
 }
 
