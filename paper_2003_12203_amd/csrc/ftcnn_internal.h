@@ -161,7 +161,12 @@ inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0 && g.R * g.S <= 409
 // Positions per tile of the channels-last copy (128 bytes of one channel) and channels per
 // tile (64 for bf16 when that still leaves 512 tiles: a stored position is then one 128-byte
 // line).
-inline int prep_tile_positions(const Geom &g) { return g.dtype == FTCNN_F32 ? 32 : 64; }
+// positions per tile of the channels-last copy: eight 16-byte vectors of a channel row, or seven
+// when H*W is not a multiple of the vector (each row segment then starts inside a vector)
+inline int prep_tile_positions(const Geom &g) {
+    const int vec = g.dtype == FTCNN_F32 ? 4 : 8;
+    return ((long long)g.H * g.W) % vec == 0 ? 8 * vec : 7 * vec;
+}
 inline int prep_tile_channels(const Geom &g) {
     const long long hw_tiles = ((long long)g.H * g.W + prep_tile_positions(g) - 1) / prep_tile_positions(g);
     return g.dtype == FTCNN_BF16 && g.C % 64 == 0 && (g.C / 64) * hw_tiles >= 512 ? 64 : 32;
