@@ -126,11 +126,10 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
         CocTile &co = pl->co;
         co.tx = g.F >= 24 ? 32 : (g.F >= 12 ? 16 : 8);
         co.ty = nt / co.tx < g.E ? nt / co.tx : g.E;
-        auto window = [&](int ty) { return (size_t)((ty - 1) * g.U + g.R) * ((co.tx - 1) * g.U + g.S); };
-        while (co.ty > 1 && 2 * sizeof(double) * window(co.ty) > lds) co.ty /= 2;
-        if (pl->prep_ns == 1 && EF * K >= (1LL << 20) && 2 * sizeof(double) * window(co.ty) <= lds) {
+        while (co.ty > 1 && coc_channel_bytes(g, co.ty, co.tx) > lds) co.ty /= 2;
+        if (pl->prep_ns == 1 && EF * K >= (1LL << 20) && coc_channel_bytes(g, co.ty, co.tx) <= lds) {
             pl->co_in_conv = true;
-            const size_t cc = lds / (2 * sizeof(double) * window(co.ty));
+            const size_t cc = lds / coc_channel_bytes(g, co.ty, co.tx);
             co.cc = (int)(cc < 8 ? cc : 8);
             co.tiles_x = (int)ceil_div(g.F, co.tx);
             co.tiles = (int)(ceil_div(g.E, co.ty) * co.tiles_x);

@@ -53,10 +53,12 @@ __device__ inline void combine_block(const Geom &g, const CdSrc &src, double *__
     }
 }
 
-// One CoC workgroup (blk < tiles * groups * ns), using lds (2 * cc * window
-// doubles).  Writes slice (group * ns + split) of copart [groups * ns][3][E*F]:
-// the share of Co5, Co6, Co7 at the tile's positions of one channel range and
-// one image range.  Each thread sums its taps in the fixed order (channel, r, s).
+// One CoC workgroup (blk < tiles * groups * ns), using lds (cc channels of
+// coc_channel_bytes).  Writes slice (group * ns + split) of copart
+// [groups * ns][3][E*F]: the share of Co5, Co6, Co7 at the tile's positions of
+// one channel range and one image range.  Each thread sums its taps in the fixed
+// order (channel, r, s).  The window is staged eight elements a thread at a
+// time (sixteen loads in flight), with the Cw1, Cw2 taps of the channels beside it.
 template <int NT>
 __device__ inline void coc_block(const Geom &g, const CocTile &ct, const CdSrc &src, const double *__restrict__ cw1,
                                  const double *__restrict__ cw2, double *__restrict__ copart, int blk,
@@ -77,37 +79,62 @@ __device__ inline void coc_block(const Geom &g, const CocTile &ct, const CdSrc &
     const int ih0 = g.U * x0 - g.P, iw0 = g.U * y0 - g.P;
     const int RS = g.R * g.S;
     double *s1 = lds, *s2 = lds + (size_t)ct.cc * plane;
+    double *w1s = s2 + (size_t)ct.cc * plane, *w2s = w1s + (size_t)ct.cc * RS;
+    // staging walk: element e = (c * PH + i) * PW + j of the window; a thread starts at e = t and
+    // steps by NT, carrying (c, i, j) along instead of dividing
+    const int sj = NT % PW, srow = NT / PW, si = srow % PH, sc = srow / PH;
+    const int tj0 = t % PW, trow0 = t / PW, ti0 = trow0 % PH, tc0 = trow0 / PH;
     double c5 = 0.0, c6 = 0.0, c7 = 0.0;
     for (int cb = c0; cb < c1; cb += ct.cc) {
         const int nc = ct.cc < c1 - cb ? ct.cc : c1 - cb;
+        const int total = nc * plane;
         __syncthreads();   // the previous group's window is no longer read
-        for (int e = t; e < nc * plane; e += NT) {
-            const int c = e / plane, rem = e - c * plane;
-            const int i = rem / PW, j = rem - (rem / PW) * PW;
-            const int ih = ih0 + i, iw = iw0 + j;
-            double a1 = 0.0, a2 = 0.0;
-            if ((unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W) {
-                const long long idx = ((long long)(cb + c) * g.H + ih) * g.W + iw;
-                a1 = p1[idx];
-                a2 = p2[idx];
+        int c = tc0, i = ti0, j = tj0;
+        for (int e0 = 0; e0 < total; e0 += 8 * NT) {
+            double a1[8], a2[8];
+            bool ok[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int ih = ih0 + i, iw = iw0 + j;
+                ok[u] = c < nc && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                const long long idx = ok[u] ? ((long long)(cb + c) * g.H + ih) * g.W + iw : 0;
+                a1[u] = p1[idx];
+                a2[u] = p2[idx];
+                j += sj;
+                i += si;
+                c += sc;
+                if (j >= PW) { j -= PW; ++i; }
+                if (i >= PH) { i -= PH; ++c; }
             }
-            s1[e] = a1;
-            s2[e] = a2;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int e = e0 + u * NT + t;
+                if (e < total) {
+                    s1[e] = ok[u] ? a1[u] : 0.0;
+                    s2[e] = ok[u] ? a2[u] : 0.0;
+                }
+            }
+        }
+        for (int e = t; e < nc * RS; e += NT) {
+            w1s[e] = cw1[(long long)cb * RS + e];
+            w2s[e] = cw2[(long long)cb * RS + e];
         }
         __syncthreads();
         if (mine) {
-            for (int c = 0; c < nc; ++c) {
-                const double *w1 = cw1 + (long long)(cb + c) * RS, *w2 = cw2 + (long long)(cb + c) * RS;
-                const double *r1 = s1 + c * plane + tyi * g.U * PW + txi * g.U;
-                const double *r2 = s2 + c * plane + tyi * g.U * PW + txi * g.U;
-                for (int r = 0; r < g.R; ++r)
+            const int base = tyi * g.U * PW + txi * g.U;
+            for (int cc = 0; cc < nc; ++cc) {
+                const double *r1 = s1 + cc * plane + base, *r2 = s2 + cc * plane + base;
+                const double *v1 = w1s + cc * RS, *v2 = w2s + cc * RS;
+                for (int r = 0; r < g.R; ++r) {
+#pragma unroll 4
                     for (int s = 0; s < g.S; ++s) {
                         const double d1 = r1[r * PW + s], d2 = r2[r * PW + s];
-                        const double v1 = w1[r * g.S + s], v2 = w2[r * g.S + s];
-                        c5 = fma(d1, v1, c5);
-                        c6 = fma(d1, v2, c6);
-                        c7 = fma(d2, v1, c7);
+                        const double w1 = v1[r * g.S + s], w2 = v2[r * g.S + s];
+                        c5 = fma(d1, w1, c5);
+                        c6 = fma(d1, w2, c6);
+                        c7 = fma(d2, w1, c7);
                     }
+                }
             }
         }
     }

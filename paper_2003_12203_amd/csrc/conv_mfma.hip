@@ -908,8 +908,7 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
             if (eb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
             e.aux_blocks = (int)eb;
         }
-        if (e.aux_kind == 2 && e.co_slices > 0 && (size_t)2 * e.co.cc * ((e.co.ty - 1) * g.U + g.R) * ((e.co.tx - 1) * g.U + g.S) *
-                                       sizeof(double) > C::LDS_BYTES)
+        if (e.aux_kind == 2 && e.co_slices > 0 && (size_t)e.co.cc * coc_channel_bytes(g, e.co.ty, e.co.tx) > C::LDS_BYTES)
             return hipErrorInvalidValue;   // the plan sized the CoC window for this tile's LDS
         if (e.aux_kind != 0 && e.aux_blocks > 0) {
             // all extra workgroups first: they start on every CU at once and are done while the

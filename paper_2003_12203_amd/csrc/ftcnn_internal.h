@@ -36,6 +36,12 @@ struct CocTile {
     int comb_blocks;
     int ns;
 };
+// LDS one channel of a CoC workgroup takes: its input window of Cd1 and Cd2 for a
+// ty x tx tile of output positions, and its R*S taps of Cw1 and Cw2 (float64)
+inline size_t coc_channel_bytes(const Geom &g, int ty, int tx) {
+    const size_t window = (size_t)((ty - 1) * g.U + g.R) * ((tx - 1) * g.U + g.S);
+    return 2 * sizeof(double) * (window + (size_t)g.R * g.S);
+}
 
 // Split counts and workspace offsets shared by every call on one layer.
 struct Plan {
