@@ -298,7 +298,7 @@ def measured_traffic():
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     h = hashlib.sha256()
-    for f in ("conv_mfma.hip", "ftcnn_internal.h"):
+    for f in ("conv_mfma.hip", "ftcnn_internal.h", "coc_tile.h", "encode_block.h"):
         with open(os.path.join(ROOT, "paper_2003_12203_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     if kv.get("source_sha256") != h.hexdigest():

@@ -117,9 +117,11 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
         long long most = g.N / min_imgs;
         most = most > 16 ? 16 : (most < 1 ? 1 : most);
         pl->prep_ns = clampi(ceil_div(1024, tiles), 1, most);
-        // Co5..Co7 in extra workgroups of the convolution launch, in its threads and LDS, for
-        // layers with many taps to evaluate (E*F*K of at least 1M) and unsplit input checksums;
-        // on the others the final launch evaluates the taps itself in a few microseconds
+        // Co5..Co7 in extra workgroups of the convolution launch, in its threads and LDS, where
+        // they hide behind the matrix-core tiles: on layers with many taps to evaluate (E*F*K of
+        // at least 1M; one pass per image range when the input checksums come split) and on
+        // every layer whose input checksums are whole.  On the others (small and split) the
+        // final launch evaluates the taps itself.
         int nt = 0;
         size_t lds = 0;
         conv_tile_shape(g, &nt, &lds);
@@ -127,7 +129,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
         co.tx = g.F >= 24 ? 32 : (g.F >= 12 ? 16 : 8);
         co.ty = nt / co.tx < g.E ? nt / co.tx : g.E;
         while (co.ty > 1 && coc_channel_bytes(g, co.ty, co.tx) > lds) co.ty /= 2;
-        if (pl->prep_ns == 1 && EF * K >= (1LL << 20) && coc_channel_bytes(g, co.ty, co.tx) <= lds) {
+        if ((pl->prep_ns == 1 || EF * K >= (1LL << 20)) && coc_channel_bytes(g, co.ty, co.tx) <= lds) {
             pl->co_in_conv = true;
             const size_t cc = lds / coc_channel_bytes(g, co.ty, co.tx);
             co.cc = (int)(cc < 8 ? cc : 8);

@@ -23,13 +23,6 @@
 
 namespace ftcnn {
 
-// Cd1 or Cd2 at element i: the image-split partials (stride apart) added in split order.
-__device__ inline double cd_at(const double *__restrict__ p, long long stride, int ns, long long i) {
-    double a = p[i];
-    for (int s = 1; s < ns; ++s) a += p[(long long)s * stride + i];
-    return a;
-}
-
 // Sources of Cd1 and Cd2 for the extra workgroups: final arrays (ns = 1) or
 // image-split partials [ns][2][Ch*H*W] (p2 = p1 + Ch*H*W, stride = 2*Ch*H*W).
 struct CdSrc {
@@ -38,19 +31,48 @@ struct CdSrc {
     int ns;
 };
 
-// One combine workgroup: 2*NT consecutive elements of Cd1 and Cd2.
+// One combine workgroup: 2*NT consecutive elements of Cd1 and Cd2, each the sum of
+// its ns image-range partials added in range order; four ranges of loads (sixteen
+// values a thread) are in flight at a time.
 template <int NT>
 __device__ inline void combine_block(const Geom &g, const CdSrc &src, double *__restrict__ cd1,
                                      double *__restrict__ cd2, int blk) {
-    const long long base = (long long)blk * 2 * NT;
+    const long long base = (long long)blk * 2 * NT + threadIdx.x;
+    long long idx[2];
+    bool in[2];
+    double a[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const long long i = base + u * NT + threadIdx.x;
-        if (i < g.CHW) {
-            cd1[i] = cd_at(src.p1, src.stride, src.ns, i);
-            cd2[i] = cd_at(src.p2, src.stride, src.ns, i);
-        }
+    for (int e = 0; e < 2; ++e) {
+        idx[e] = base + e * NT;
+        in[e] = idx[e] < g.CHW;
+        if (!in[e]) idx[e] = 0;
     }
+    for (int s0 = 0; s0 < src.ns; s0 += 4) {
+        double x[4][2][2];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const long long off = (long long)(s0 + u < src.ns ? s0 + u : 0) * src.stride;
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                x[u][e][0] = src.p1[off + idx[e]];
+                x[u][e][1] = src.p2[off + idx[e]];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (s0 + u < src.ns)
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    a[e][0] += x[u][e][0];
+                    a[e][1] += x[u][e][1];
+                }
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+        if (in[e]) {
+            cd1[idx[e]] = a[e][0];
+            cd2[idx[e]] = a[e][1];
+        }
 }
 
 // One CoC workgroup (blk < tiles * groups * ns), using lds (cc channels of

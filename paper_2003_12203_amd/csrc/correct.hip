@@ -660,21 +660,23 @@ __device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double 
     int r = rem / g.S, s = rem - r * g.S;
     const int dch = TPP / RS, drem = TPP - dch * RS, dr = drem / g.S, ds = drem - dr * g.S;
     const int ih0 = g.U * x - g.P, iw0 = g.U * y - g.P;
-    // branch-free taps, four in flight: a tap in the zero padding reads element 0 and selects 0
-    constexpr int U4 = 4;
-    int k = lane;
-    for (; k + (U4 - 1) * TPP < g.K; k += U4 * TPP) {
-        double d1[U4], d2[U4], w1[U4], w2[U4], ok[U4];
+    // branch-free taps, eight in flight: a tap past K or in the zero padding reads element 0
+    // and selects 0 (the taps are added in the order k = lane, lane + TPP, ...)
+    constexpr int U = 8;
+    for (int k = lane; k < g.K; k += U * TPP) {
+        double d1[U], d2[U], w1[U], w2[U];
+        bool ok[U];
 #pragma unroll
-        for (int u = 0; u < U4; ++u) {
+        for (int u = 0; u < U; ++u) {
+            const int kk = k + u * TPP;
             const int ih = ih0 + r, iw = iw0 + s;
-            const bool in = ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
-            const long long off = in ? ((long long)ch * g.H + ih) * g.W + iw : 0;
+            ok[u] = kk < g.K && ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
+            const long long off = ok[u] ? ((long long)ch * g.H + ih) * g.W + iw : 0;
+            const int kw = kk < g.K ? kk : 0;
             d1[u] = c.cd1[off];
             d2[u] = c.cd2[off];
-            w1[u] = c.cw1[k + u * TPP];
-            w2[u] = c.cw2[k + u * TPP];
-            ok[u] = in ? 1.0 : 0.0;
+            w1[u] = c.cw1[kw];
+            w2[u] = c.cw2[kw];
             s += ds;
             r += dr;
             ch += dch;
@@ -682,27 +684,12 @@ __device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double 
             if (r >= g.R) { r -= g.R; ++ch; }
         }
 #pragma unroll
-        for (int u = 0; u < U4; ++u) {
-            const double a1 = ok[u] != 0.0 ? d1[u] : 0.0, a2 = ok[u] != 0.0 ? d2[u] : 0.0;
-            c5 = fma(a1, w1[u], c5);
-            c6 = fma(a1, w2[u], c6);
-            c7 = fma(a2, w1[u], c7);
-        }
-    }
-    for (; k < g.K; k += TPP) {
-        const int ih = ih0 + r, iw = iw0 + s;
-        if ((unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W) {
-            const long long off = ((long long)ch * g.H + ih) * g.W + iw;
-            const double d1 = c.cd1[off], d2 = c.cd2[off];
-            c5 = fma(d1, c.cw1[k], c5);
-            c6 = fma(d1, c.cw2[k], c6);
-            c7 = fma(d2, c.cw1[k], c7);
-        }
-        s += ds;
-        r += dr;
-        ch += dch;
-        if (s >= g.S) { s -= g.S; ++r; }
-        if (r >= g.R) { r -= g.R; ++ch; }
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) {
+                c5 = fma(d1[u], w1[u], c5);
+                c6 = fma(d1[u], w2[u], c6);
+                c7 = fma(d2[u], w1[u], c7);
+            }
     }
 }
 
@@ -741,23 +728,44 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
             // the workspace holds)
             const int groups = min(c.rep->reserved[1], max_groups);
             if (groups > 0) {
-                for (int s = lane; s < groups; s += TPP) {
-                    const double *ps = copart + (size_t)s * 3 * g.EF + p;
-                    v[4] += ps[0];
-                    v[5] += ps[g.EF];
-                    v[6] += ps[2 * (size_t)g.EF];
+                for (int s0 = lane; s0 < groups; s0 += 4 * TPP) {
+                    double x[4][3];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int s = s0 + u * TPP;
+                        const double *ps = copart + (size_t)(s < groups ? s : 0) * 3 * g.EF + p;
+                        x[u][0] = ps[0];
+                        x[u][1] = ps[g.EF];
+                        x[u][2] = ps[2 * (size_t)g.EF];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (s0 + u * TPP < groups) {
+                            v[4] += x[u][0];
+                            v[5] += x[u][1];
+                            v[6] += x[u][2];
+                        }
                 }
             } else {
                 const int x = p / g.F;
                 coc_taps<T, TPP>(c, lane, x, p - x * g.F, v[4], v[5], v[6]);
             }
         }
-        for (int s = lane; s < splits; s += TPP) {
-            const double *ps = part + (size_t)s * 4 * g.EF + p;
-            v[0] += ps[0];
-            v[1] += ps[g.EF];
-            v[2] += ps[2 * (size_t)g.EF];
-            v[3] += ps[3 * (size_t)g.EF];
+        // four slices of loads in flight, added in slice order
+        for (int s0 = lane; s0 < splits; s0 += 4 * TPP) {
+            double x[4][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int s = s0 + u * TPP;
+                const double *ps = part + (size_t)(s < splits ? s : 0) * 4 * g.EF + p;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) x[u][i] = ps[i * (size_t)g.EF];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (s0 + u * TPP < splits)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] += x[u][i];
         }
     }
     if constexpr (TPP > 1) {

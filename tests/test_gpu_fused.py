@@ -229,6 +229,12 @@ SPLIT_SHAPES = [
     (64, 64, 7, 48, 3, 1, 1, "bf16"),
     (96, 64, 6, 70, 3, 2, 1, "bf16"),
 ]
+# split images on layers with E*F*K of at least 1M: Co5..Co7 in the convolution launch, one pass
+# per image range
+SPLIT_COC_SHAPES = [
+    (32, 32, 64, 32, 3, 1, 1, "f32"),
+    (64, 64, 48, 64, 3, 1, 1, "bf16"),
+]
 
 
 def _split_spec(shape):
@@ -236,7 +242,8 @@ def _split_spec(shape):
     return wl.LayerSpec("split", n, ch, h, h, m, r, r, u, p, dtype)
 
 
-@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "n{}-c{}-h{}-m{}-r{}-u{}-{}".format(*s[:6], s[7]))
+@pytest.mark.parametrize("shape", SPLIT_SHAPES + SPLIT_COC_SHAPES,
+                         ids=lambda s: "n{}-c{}-h{}-m{}-r{}-u{}-{}".format(*s[:6], s[7]))
 def test_image_split_encode_integer_exact(shape):
     """Integer data: the combined image-range partials are exactly Cd1, Cd2, and the Co5..Co7
     partial products of the convolution launch add up exactly to the summations of O."""
