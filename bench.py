@@ -59,6 +59,11 @@ def parse():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run a plain fp32 device copy of this size first (counter calibration)")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--schemes", action="store_true",
+                    help="instead of the benchmark: the cost of every correction workflow (CoC, RC, ClC, FC, "
+                         "recomputation) on each distinct layer, and the layerwise RC/ClC choice (one JSON "
+                         "line per layer)")
+    ap.add_argument("--scheme-reps", type=int, default=10)
     return ap.parse_args()
 
 
@@ -81,6 +86,52 @@ class LayerRun:
                       "y": int(d[3] * F), "kind": "add", "value": FAULT_VALUE}
 
 
+def scheme_table(args, cfg, runs, ft, torch):
+    """Per distinct layer: the unprotected convolution, the error-free protected step (its excess
+    is CoC-D), and each correction workflow of Sec. 4.3 on a fault pattern it must handle (the
+    excess over the error-free step), all medians in microseconds; then the RC/ClC switch the
+    paper's rule picks from those times."""
+    import statistics
+
+    from paper_2003_12203_amd import schemes
+
+    seen = set()
+    for li, r in enumerate(runs):
+        s = cfg.layers[li]
+        key = (s.n, s.ch, s.h, s.w, s.m, s.r, s.s, s.stride, s.pad, s.dtype)
+        if key in seen:
+            continue
+        seen.add(key)
+        L = r.lay
+        ts = []
+        L.conv_ws(r.D, r.W, r.O)
+        for _ in range(args.scheme_reps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record()
+            L.conv_ws(r.D, r.W, r.O)
+            ev[1].record()
+            ev[1].synchronize()
+            ts.append(ev[0].elapsed_time(ev[1]) * 1e3)
+        t_conv = statistics.median(ts)
+        res = schemes.measure(L, r.D, r.W, reps=args.scheme_reps)
+        base = res["error-free"]["us"]
+        flows = {}
+        for name, v in res.items():
+            if name == "error-free":
+                continue
+            flows[name] = {"extra_us": round(v["us"] - base, 2), "resolved": v["resolved"],
+                           "as_expected": tuple(v["resolved"]) == schemes.WORKFLOWS[name][3]}
+        line = {"workload": cfg.name, "layer": s.name, "dtype": s.dtype, "conv_us": round(t_conv, 2),
+                "protected_us": round(base, 2), "coc_d_us": round(base - t_conv, 2), "workflows": flows}
+        t = {k: v["us"] for k, v in res.items()}
+        if all(k in t for k in schemes.WORKFLOWS):
+            c = schemes.rc_clc_policy(t, s.n * s.ch * s.h * s.w, s.m * s.ch * s.r * s.s)
+            line["policy"] = {"rc_on": c.rc_on, "clc_on": c.clc_on, "rc_gain_us": round(c.rc_gain, 2),
+                              "rc_loss_us": round(c.rc_loss, 2), "clc_gain_us": round(c.clc_gain, 2),
+                              "clc_loss_us": round(c.clc_loss, 2)}
+        print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -99,6 +150,9 @@ def main():
     cfg = {"alexnet": wl.config(1), "vgg19": wl.config(2), "vgg19_bf16": wl.vgg19_bf16(),
            "resnet18": wl.config(3), "darknet19": wl.config(4)}[args.workload]
     runs = [LayerRun(cfg, li, ft, torch) for li in range(len(cfg.layers))]
+    if args.schemes:
+        scheme_table(args, cfg, runs, ft, torch)
+        return
     dtype = cfg.layers[0].dtype
     peak = MFMA_PEAK[dtype]
     nl = len(runs)
