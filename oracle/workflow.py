@@ -33,7 +33,11 @@ Readings where the paper is silent (all shared with the HIP library):
   at p, and if the output agrees with the fresh ones p is closed as a checksum
   fault with no repair; otherwise the chain continues with the fresh ones;
 * positions left unresolved trigger a recomputation of the whole layer
-  (Sec. 4.1.1).
+  (Sec. 4.1.1);
+* with a bias (Sec. 5.1) the output is eq. (1) plus Bias[m], the checksums stay
+  those of the convolution, and every summation has the bias share of Table 5
+  subtracted before it is compared or used in a repair (with the paper's index
+  sums read as sums of the block weights n + wbase and m + wbase).
 """
 from __future__ import annotations
 
@@ -187,6 +191,46 @@ def col_checksums(ck: Checksums, D: np.ndarray, stride: int, pad: int):
     return (checksum_conv(D, ck.cw1, stride, pad)[:, 0], checksum_conv(D, ck.cw2, stride, pad)[:, 0])
 
 
+@dataclasses.dataclass
+class BiasTerms:
+    """The bias shares of the output summations (Sec. 5.1, Table 5), precomputed from Bias[m]:
+    with wn = sum_n (n + wbase), b1 = sum_m Bias[m] and b2 = sum_m (m + wbase) Bias[m],
+    So1[m] carries N Bias[m], So3[m] wn Bias[m], So2[n] b1, So4[n] b2, So5 N b1, So6 N b2 and
+    So7 wn b1."""
+    bias: np.ndarray
+    wn: float
+    b1: float
+    b2: float
+    N: int
+
+    @staticmethod
+    def make(bias: Optional[np.ndarray], N: int, M: int, wbase: int) -> "BiasTerms":
+        b = np.zeros(M) if bias is None else np.asarray(bias, dtype=np.float64).reshape(M)
+        wn = float(np.sum(np.arange(N, dtype=np.float64) + wbase))
+        wm = np.arange(M, dtype=np.float64) + wbase
+        return BiasTerms(b, wn, float(b.sum()), float((wm * b).sum()), N)
+
+    @property
+    def s5(self) -> float:
+        return self.N * self.b1
+
+    @property
+    def s6(self) -> float:
+        return self.N * self.b2
+
+    @property
+    def s7(self) -> float:
+        return self.wn * self.b1
+
+    @property
+    def s1(self) -> np.ndarray:
+        return self.N * self.bias
+
+    @property
+    def s3(self) -> np.ndarray:
+        return self.wn * self.bias
+
+
 # ----------------------------------------------------------------------------
 # detection
 # ----------------------------------------------------------------------------
@@ -201,11 +245,13 @@ def bad(d, Q, scale):
         return np.logical_or(~np.isfinite(d), np.abs(d) > scale * Q)
 
 
-def verify(O: np.ndarray, co5: np.ndarray, K: int, dtype: str, policy: Policy):
-    """CoC-D (Sec. 3.6): So5 = sum_{n,m} O_nm compared with Co5 at every position.
+def verify(O: np.ndarray, co5: np.ndarray, K: int, dtype: str, policy: Policy,
+           bt: Optional[BiasTerms] = None):
+    """CoC-D (Sec. 3.6): So5 = sum_{n,m} O_nm, less its bias share (Sec. 5.1), compared with
+    Co5 at every position.
 
-    Returns (So5, So6, So7, Q5, flags[E][F]).  So6 and So7 are the weighted
-    summations of Sec. 3.6; they are reported for parity checks only.
+    Returns (So5, So6, So7, Q5, flags[E][F]), the summations as taken from O.  So6 and So7
+    are the weighted summations of Sec. 3.6; they are reported for parity checks only.
     """
     N, M = O.shape[:2]
     wn = (np.arange(N, dtype=np.float64) + policy.wbase)[:, None, None, None]
@@ -215,7 +261,8 @@ def verify(O: np.ndarray, co5: np.ndarray, K: int, dtype: str, policy: Policy):
         so6 = (O * wm).sum(axis=(0, 1))
         so7 = (O * wn).sum(axis=(0, 1))
         q5 = np.sqrt((O * O).sum(axis=(0, 1)))
-        flags = bad(co5 - so5, q5, tol_scale(K, dtype, policy.kappa))
+        share = bt.s5 if bt is not None else 0.0
+        flags = bad(co5 - (so5 - share), q5, tol_scale(K, dtype, policy.kappa))
     return so5, so6, so7, q5, flags
 
 
@@ -224,7 +271,7 @@ def verify(O: np.ndarray, co5: np.ndarray, K: int, dtype: str, policy: Policy):
 # ----------------------------------------------------------------------------
 
 class _Layer:
-    def __init__(self, O, D, W, ck, stride, pad, dtype, policy):
+    def __init__(self, O, D, W, ck, stride, pad, dtype, policy, bt=None):
         self.O, self.D, self.W, self.ck = O, D, W, ck
         self.stride, self.pad, self.dtype, self.pol = stride, pad, dtype, policy
         self.N, self.M, self.E, self.F = O.shape
@@ -233,6 +280,7 @@ class _Layer:
         self.wn = np.arange(self.N, dtype=np.float64) + policy.wbase
         self.wm = np.arange(self.M, dtype=np.float64) + policy.wbase
         self._rows = self._cols = self._fresh = None
+        self.bt = bt if bt is not None else BiasTerms.make(None, self.N, self.M, policy.wbase)
 
     # lazily computed per-layer checksum arrays (the paper computes them on demand, Sec. 4.3)
     def rows(self):
@@ -265,10 +313,15 @@ class _Layer:
             return (Op.sum(), t6.sum(), t7.sum(),
                     np.sqrt((Op * Op).sum()), np.sqrt((t6 * t6).sum()), np.sqrt((t7 * t7).sum()))
 
+    def adjusted(self, s5, s6, s7):
+        """So5, So6, So7 less their bias shares (Sec. 5.1, Table 5)."""
+        return s5 - self.bt.s5, s6 - self.bt.s6, s7 - self.bt.s7
+
     def consistent(self, x, y, co):
         s5, s6, s7, q5, q6, q7 = self.block_sums_at(x, y)
-        return not (bad(co[0] - s5, q5, self.scale) or bad(co[1] - s6, q6, self.scale)
-                    or bad(co[2] - s7, q7, self.scale))
+        a5, a6, a7 = self.adjusted(s5, s6, s7)
+        return not (bad(co[0] - a5, q5, self.scale) or bad(co[1] - a6, q6, self.scale)
+                    or bad(co[2] - a7, q7, self.scale))
 
     def legal(self, r, hi):
         if not np.isfinite(r):
@@ -279,25 +332,26 @@ class _Layer:
         return int(i)
 
     def element(self, n, m, x, y):
-        """Eq. (1) for one element (the RECOMPUTE repair option)."""
+        """Eq. (1) for one element, plus its bias (the RECOMPUTE repair option)."""
         return core.conv_points(self.D, self.W, self.stride, self.pad,
-                                np.array([[n, m, x, y]], dtype=np.int32))[0]
+                                np.array([[n, m, x, y]], dtype=np.int32))[0] + self.bt.bias[m]
 
     def excl_row(self, co1m, m, i, x, y):
-        """Co1[m] minus the other blocks of column m (exclusive sum over n != i)."""
+        """Co1[m] minus the other blocks of column m (exclusive sum over n != i), the sum less
+        the bias share of So1[m]."""
         col = self.O[:, m, x, y]
         with np.errstate(invalid="ignore", over="ignore"):
-            return co1m - np.delete(col, i).sum()
+            return co1m - (np.delete(col, i).sum() - self.bt.s1[m])
 
     def excl_col(self, co2n, n, j, x, y):
         row = self.O[n, :, x, y]
         with np.errstate(invalid="ignore", over="ignore"):
-            return co2n - np.delete(row, j).sum()
+            return co2n - (np.delete(row, j).sum() - self.bt.b1)
 
     def excl_all(self, co5, i, j, x, y):
         others = np.delete(self.O[:, :, x, y].reshape(-1), i * self.M + j)
         with np.errstate(invalid="ignore", over="ignore"):
-            return co5 - others.sum()
+            return co5 - (others.sum() - self.bt.s5)
 
     def apply(self, fixes, x, y):
         """Write repaired values (rounded to the dtype); return the previous values."""
@@ -332,8 +386,8 @@ class _Layer:
             t3 = col * self.wn[:, None]
             s3 = t3.sum(axis=0)
             q1 = np.sqrt((col * col).sum(axis=0))
-            d1 = co1[:, x, y] - s1
-            d3 = co3[:, x, y] - s3
+            d1 = co1[:, x, y] - (s1 - self.bt.s1)
+            d3 = co3[:, x, y] - (s3 - self.bt.s3)
         mset = [m for m in range(self.M) if bad(d1[m], q1[m], self.scale)]
         return co1[:, x, y], d1, d3, mset
 
@@ -345,8 +399,8 @@ class _Layer:
             t4 = row * self.wm[None, :]
             s4 = t4.sum(axis=1)
             q2 = np.sqrt((row * row).sum(axis=1))
-            d2 = co2[:, x, y] - s2
-            d4 = co4[:, x, y] - s4
+            d2 = co2[:, x, y] - (s2 - self.bt.b1)
+            d4 = co4[:, x, y] - (s4 - self.bt.b2)
         nset = [n for n in range(self.N) if bad(d2[n], q2[n], self.scale)]
         return co2[:, x, y], d2, d4, nset
 
@@ -424,6 +478,7 @@ class _Layer:
         ck = self.ck
         co = (ck.co5[x, y], ck.co6[x, y], ck.co7[x, y])
         s5, s6, s7, q5, q6, q7 = self.block_sums_at(x, y)
+        s5, s6, s7 = self.adjusted(s5, s6, s7)
         d = (co[0] - s5, co[1] - s6, co[2] - s7)
         agree = [not bad(d[0], q5, self.scale), not bad(d[1], q6, self.scale),
                  not bad(d[2], q7, self.scale)]
@@ -452,7 +507,7 @@ class _Layer:
 
 
 def correct(O: np.ndarray, D: np.ndarray, W: np.ndarray, ck: Checksums, flags: np.ndarray,
-            stride: int, pad: int, dtype: str, policy: Policy) -> Report:
+            stride: int, pad: int, dtype: str, policy: Policy, bt: Optional[BiasTerms] = None) -> Report:
     """Correction module of the multischeme workflow (Sec. 4.3), O repaired in place."""
     rep = Report()
     E, F = O.shape[2:]
@@ -462,7 +517,7 @@ def correct(O: np.ndarray, D: np.ndarray, W: np.ndarray, ck: Checksums, flags: n
     if not rep.detected:
         rep.status = STATUS_CLEAN
         return rep
-    L = _Layer(O, D, W, ck, stride, pad, dtype, policy)
+    L = _Layer(O, D, W, ck, stride, pad, dtype, policy, bt)
     for p in rep.flagged:
         x, y = divmod(p, F)
         scheme, fixes = L.resolve(x, y)
@@ -492,7 +547,8 @@ class LayerResult:
 
 def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
             policy: Optional[Policy] = None, faults: Sequence[Fault] = (),
-            O_in: Optional[np.ndarray] = None, after_encode=None) -> LayerResult:
+            O_in: Optional[np.ndarray] = None, after_encode=None,
+            bias: Optional[np.ndarray] = None) -> LayerResult:
     """One protected layer: encode, convolve, checksum convs, verify, correct, recompute.
 
     ``after_encode(D, W, ck)`` may corrupt copies of D, W or the input
@@ -500,13 +556,19 @@ def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
     the convolution and everything after it then see the corrupted data.
     ``O_in`` replaces the oracle's own convolution (decision-oracle mode: the
     caller supplies an output, e.g. a faulted one, and the workflow decides on
-    it).  ``O_clean`` is always the output of the uncorrupted inputs.
+    it).  ``O_clean`` is always the output of the uncorrupted inputs.  ``bias`` [M] is added
+    to every output block O[n][m] (Sec. 5.1).
     """
     policy = policy or Policy()
     D = np.array(D, dtype=np.float64)
     W = np.array(W, dtype=np.float64)
     K = W.shape[1] * W.shape[2] * W.shape[3]
-    O_clean = store(core.conv(D, W, stride, pad), dtype)
+    bt = BiasTerms.make(bias, D.shape[0], W.shape[0], policy.wbase)
+
+    def conv_b(D_, W_):
+        return store(core.conv(D_, W_, stride, pad) + bt.bias[None, :, None, None], dtype)
+
+    O_clean = conv_b(D, W)
     cw1, cw2 = encode(W, policy.wbase)  # before the application (Sec. 4.2)
     cd1, cd2 = encode(D, policy.wbase)  # before the convolution (Sec. 3.3)
     ck = Checksums(cd1, cd2, cw1, cw2)
@@ -518,15 +580,15 @@ def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
     if O_in is not None:
         O = np.array(O_in, dtype=np.float64)
     elif touched:
-        O = store(core.conv(D, W, stride, pad), dtype)
+        O = conv_b(D, W)
     else:
         O = O_clean.copy()
     apply_faults(O, dtype, faults)
     O_faulty = O.copy()
-    so5, so6, so7, q5, flags = verify(O, ck.co5, K, dtype, policy)
-    rep = correct(O, D, W, ck, flags, stride, pad, dtype, policy)
+    so5, so6, so7, q5, flags = verify(O, ck.co5, K, dtype, policy, bt)
+    rep = correct(O, D, W, ck, flags, stride, pad, dtype, policy, bt)
     if rep.status == STATUS_NEEDS_RECOMPUTE:
-        O[...] = store(core.conv(D, W, stride, pad), dtype)
-        *_, flags2 = verify(O, ck.co5, K, dtype, policy)
+        O[...] = conv_b(D, W)
+        *_, flags2 = verify(O, ck.co5, K, dtype, policy, bt)
         rep.status = STATUS_FAILED if flags2.any() else STATUS_RECOMPUTED
     return LayerResult(O, O_faulty, O_clean, ck, (so5, so6, so7, q5), flags, rep)
