@@ -64,11 +64,14 @@ def parse():
                          "recomputation) on each distinct layer, and the layerwise RC/ClC choice (one JSON "
                          "line per layer)")
     ap.add_argument("--scheme-reps", type=int, default=10)
+    ap.add_argument("--bias", action="store_true",
+                    help="give every layer a seeded bias (Sec. 5.1): the output carries it and every check "
+                         "applies its shares (the workloads themselves have none)")
     return ap.parse_args()
 
 
 class LayerRun:
-    def __init__(self, cfg, li, ft, torch):
+    def __init__(self, cfg, li, ft, torch, bias=False):
         import workloads as wl
         self.spec = spec = cfg.layers[li]
         self.name = spec.name
@@ -79,6 +82,9 @@ class LayerRun:
         self.W = torch.from_numpy(wl.gen_w(cfg, li)).to(tdt).cuda()
         self.O = self.lay.empty_output()
         self.lay.encode_weights(self.W)
+        if bias:
+            b = np.random.default_rng([12203, cfg.cid, li, 5]).uniform(-0.1, 0.1, size=spec.m)
+            self.lay.set_bias(torch.from_numpy(b.astype(np.float32)).cuda())
         E, F = self.lay.E, self.lay.F
         self.flops = 2.0 * spec.n * spec.m * E * F * spec.ch * spec.r * spec.s
         d = wl.fault_draws(cfg.cid, li, 1)[0]
@@ -149,7 +155,7 @@ def main():
     torch.cuda.set_device(0)
     cfg = {"alexnet": wl.config(1), "vgg19": wl.config(2), "vgg19_bf16": wl.vgg19_bf16(),
            "resnet18": wl.config(3), "darknet19": wl.config(4)}[args.workload]
-    runs = [LayerRun(cfg, li, ft, torch) for li in range(len(cfg.layers))]
+    runs = [LayerRun(cfg, li, ft, torch, args.bias) for li in range(len(cfg.layers))]
     if args.schemes:
         scheme_table(args, cfg, runs, ft, torch)
         return
@@ -319,7 +325,8 @@ def main():
         "config": {"workload": f"{cfg.name.split('_')[0]}-{nl}conv-{'fp32' if dtype == 'f32' else 'bf16'}"
                                f"-b{cfg.layers[0].n}",
                    "batch": cfg.layers[0].n, "layers": nl,
-                   "faults_per_step": 1, "gflop_per_step": round(total_flops / 1e9, 3)},
+                   "faults_per_step": 1, "gflop_per_step": round(total_flops / 1e9, 3),
+                   **({"bias": True} if args.bias else {})},
         "error_free_tflops": round(total_flops / t_clean / 1e12, 3),
         "unprotected_tflops": round(total_flops / t_unprot / 1e12, 3),
         "overhead_error_free_pct": round((t_clean / t_unprot - 1) * 100, 2),

@@ -80,6 +80,17 @@ typedef struct {
     double *so5, *so6, *so7, *q5;   /* [E][F]       summations of O, and sqrt(sum O^2) */
     double *co1, *co3;              /* [m][E][F]    row checksums          */
     double *co2, *co4;              /* [n][E][F]    column checksums       */
+    /* Optional bias (Sec. 5.1): bias[m] (fp32, for either layer dtype) is added to every
+     * element of O[n][m] by the calls that compute O with the checksums (ftcnn_conv_fwd_sums,
+     * ftcnn_protected_conv); cb = {sum_m bias[m], sum_m (m + wbase) bias[m]}, from
+     * ftcnn_encode(which = 2), once per layer.  The checksums Co1..Co7 stay those of the
+     * convolution; every detection and correction call given a non-NULL bias subtracts the
+     * bias share of Table 5 from each summation before comparing it (N bias[m] from So1[m],
+     * (sum_n (n + wbase)) bias[m] from So3[m], cb[0] from So2[n], cb[1] from So4[n],
+     * N cb[0] from So5, N cb[1] from So6, (sum_n (n + wbase)) cb[0] from So7), and a
+     * recomputed element includes its bias.  NULL bias: no bias (cb unused). */
+    const float *bias;              /* [m]                                  */
+    double *cb;                     /* [2]                                  */
 } ftcnn_checksums;
 
 /* Correction schemes, as recorded per repaired element and per position. */
@@ -157,7 +168,9 @@ const char *ftcnn_last_error(void);
 /* Sec. 3.2 input checksums.  which = 0: X is D, c1 = Cd1 = sum_n D_n and
  * c2 = Cd2 = sum_n (n + wbase) D_n, each [ch][h][w].  which = 1: X is W,
  * c1 = Cw1, c2 = Cw2, each [ch][r][s] (computed once per layer, before the
- * application, Sec. 4.2).  float64 accumulation; deterministic. */
+ * application, Sec. 4.2).  which = 2: X is a bias (float [m]), c1 = sum_m bias[m]
+ * and c2 = sum_m (m + wbase) bias[m], one double each (the precomputed bias sums
+ * of Sec. 5.1).  float64 accumulation; deterministic. */
 int ftcnn_encode(const ftcnn_conv_desc *desc, int32_t which, const void *X,
                  double *c1, double *c2, void *workspace, hipStream_t stream);
 
@@ -166,6 +179,15 @@ int ftcnn_encode(const ftcnn_conv_desc *desc, int32_t which, const void *X,
  * fp32 accumulation, O rounded to the layer dtype (nearest even). */
 int ftcnn_conv_fwd(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                    hipStream_t stream);
+
+/* Eq. (1) plus a bias (Sec. 5.1): O[n][m][x][y] = (eq. (1)) + bias[m], added to the fp32
+ * accumulator before O is rounded to the layer dtype.  bias: device, fp32 [m].  With a
+ * workspace (ftcnn_workspace_bytes) the convolution runs through the kernels of the
+ * protected path (channels-last copies on layers whose ch is a multiple of 32), so O is
+ * bitwise that of ftcnn_conv_fwd_sums with the same bias; with NULL, through those of
+ * ftcnn_conv_fwd. */
+int ftcnn_conv_fwd_bias(const ftcnn_conv_desc *desc, const void *D, const void *W, const float *bias,
+                        void *O, void *workspace, hipStream_t stream);
 
 /* Output checksums of Sec. 3.2, as convolutions of checksum blocks, float64:
  *   FTCNN_CO1 | FTCNN_CO3: Co1 = Cd1 (x) W, Co3 = Cd2 (x) W   (reads cd1/cd2, W)

@@ -113,6 +113,11 @@ def verify_correct(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
            "ftcnn_verify_correct")
 
 
+def conv_fwd_bias(desc, D, W, bias, O, workspace=None, stream=None) -> None:
+    _check(lib().ftcnn_conv_fwd_bias(C.byref(desc), _ptr(D), _ptr(W), _ptr(bias), _ptr(O), _ptr(workspace),
+                                     _stream(stream)), "ftcnn_conv_fwd_bias")
+
+
 def conv_fwd_ws(desc, D, W, O, workspace, stream=None) -> None:
     _check(lib().ftcnn_conv_fwd_ws(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), _ptr(workspace), _stream(stream)),
            "ftcnn_conv_fwd_ws")
@@ -220,6 +225,7 @@ class Layer:
         for k in ("co5", "co6", "co7", "so5", "so6", "so7", "q5"):
             self.buf[k] = torch.zeros(EF, **f64)
         self.ck = _lib.Checksums()
+        self.bias: Optional[torch.Tensor] = None
         self._sync_ck()
         nbytes = workspace_bytes(self.desc)
         self._ws_raw = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
@@ -243,6 +249,25 @@ class Layer:
             self.buf["co4"] = torch.zeros(n * EF, dtype=torch.float64, device=dev)
         self._sync_ck()
 
+    def set_bias(self, bias: Optional[torch.Tensor], stream=None):
+        """A bias [M] added to every output block O[n][m] (Sec. 5.1), kept in fp32 on the device,
+        with its sums encoded once (ftcnn_encode, which = 2); None removes it."""
+        if bias is None:
+            self.bias = None
+            self.ck.bias = None
+            self.ck.cb = None
+            return
+        b = bias.detach().to(device=self.buf["cd1"].device, dtype=torch.float32).contiguous().reshape(-1)
+        if b.numel() != self.shape_w[0]:
+            raise FtcnnError(f"bias has {b.numel()} elements, the layer {self.shape_w[0]} filters")
+        self.bias = b
+        if "cb" not in self.buf:
+            self.buf["cb"] = torch.zeros(2, dtype=torch.float64, device=b.device)
+        cb = self.buf["cb"]
+        encode(self.desc, 2, b, cb[0:1], cb[1:2], self.workspace, stream)
+        self._sync_ck()
+        self.ck.bias = b.data_ptr()
+
     def empty_output(self) -> torch.Tensor:
         return torch.empty(self.shape_o, dtype=self.tdtype, device=self.buf["cd1"].device)
 
@@ -254,7 +279,10 @@ class Layer:
         encode(self.desc, 0, D, self.buf["cd1"], self.buf["cd2"], self.workspace, stream)
 
     def conv(self, D, W, O, stream=None):
-        conv_fwd(self.desc, D, W, O, stream)
+        if self.bias is not None:
+            conv_fwd_bias(self.desc, D, W, self.bias, O, None, stream)
+        else:
+            conv_fwd(self.desc, D, W, O, stream)
 
     def checksum_conv(self, which, D=None, W=None, stream=None):
         checksum_conv(self.desc, which, D, W, self.ck, stream)
@@ -269,17 +297,23 @@ class Layer:
         verify_correct(self.desc, D, W, O, self.ck, self.policy, self.report, self.cap, self.workspace, stream)
 
     def conv_ws(self, D, W, O, stream=None):
-        """ftcnn_conv_fwd_ws: the convolution through the protected path's kernels."""
-        conv_fwd_ws(self.desc, D, W, O, self.workspace, stream)
+        """ftcnn_conv_fwd_ws (ftcnn_conv_fwd_bias with a bias): the convolution through the
+        protected path's kernels."""
+        if self.bias is not None:
+            conv_fwd_bias(self.desc, D, W, self.bias, O, self.workspace, stream)
+        else:
+            conv_fwd_ws(self.desc, D, W, O, self.workspace, stream)
 
     def conv_sums(self, D, W, O, faults=(), stream=None, encode=False):
         """ftcnn_conv_fwd_sums; encode=True also encodes Cd1, Cd2 of D in the same pass and, on
         channels-last layers, computes the Co5..Co7 partials from them and Cw1, Cw2."""
         ck = None
-        if encode:
+        if encode or self.bias is not None:
             ck = _lib.Checksums()
-            ck.cd1, ck.cd2 = self.buf["cd1"].data_ptr(), self.buf["cd2"].data_ptr()
-            ck.cw1, ck.cw2 = self.buf["cw1"].data_ptr(), self.buf["cw2"].data_ptr()
+            if encode:
+                ck.cd1, ck.cd2 = self.buf["cd1"].data_ptr(), self.buf["cd2"].data_ptr()
+                ck.cw1, ck.cw2 = self.buf["cw1"].data_ptr(), self.buf["cw2"].data_ptr()
+            ck.bias, ck.cb = self.ck.bias, self.ck.cb   # the layer's bias goes into O
         conv_fwd_sums(self.desc, D, W, O, ck, self.report, self.cap, self.workspace, faults, stream)
 
     def verify_correct_sums(self, D, W, O, stream=None, coc=False):

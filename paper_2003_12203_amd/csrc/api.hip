@@ -184,8 +184,12 @@ int check_policy(const ftcnn_policy *p) {
 }
 
 int do_encode(const Plan &pl, int which, const void *X, double *c1, double *c2, void *ws, hipStream_t st) {
-    if (which != 0 && which != 1) return fail(FTCNN_E_ARG, "encode which = %d (0 = D, 1 = W)", which);
+    if (which < 0 || which > 2) return fail(FTCNN_E_ARG, "encode which = %d (0 = D, 1 = W, 2 = bias)", which);
     if (!X || !c1 || !c2) return fail(FTCNN_E_ARG, "encode: null pointer");
+    if (which == 2) {
+        FT_HIP(launch_bias_sums(pl, static_cast<const float *>(X), c1, c2, st), "encode bias");
+        return FTCNN_OK;
+    }
     const int splits = which == 0 ? pl.enc_splits_d : pl.enc_splits_w;
     if (splits > 1) FT_TRY(check_ws(pl, ws));
     FT_HIP(launch_encode(pl, which, X, c1, c2, ws, st), "encode");
@@ -221,10 +225,17 @@ int do_cksum(const Plan &pl, uint32_t which, const void *D, const void *W, const
     return FTCNN_OK;
 }
 
+// A bias takes its precomputed sums (ftcnn_encode, which = 2) into every check.
+int check_bias(const ftcnn_checksums *ck) {
+    if (ck && ck->bias && !ck->cb) return fail(FTCNN_E_ARG, "a bias needs its sums cb (ftcnn_encode which = 2)");
+    return FTCNN_OK;
+}
+
 int do_verify(const Plan &pl, const void *O, const ftcnn_checksums *ck, const ftcnn_policy *pol,
               ftcnn_report *rep, int32_t cap, void *ws, hipStream_t st) {
     FT_TRY(check_policy(pol));
     if (!O || !ck || !rep) return fail(FTCNN_E_ARG, "verify: null pointer");
+    FT_TRY(check_bias(ck));
     if (!ck->co5 || !ck->so5 || !ck->so6 || !ck->so7 || !ck->q5)
         return fail(FTCNN_E_ARG, "verify needs co5, so5, so6, so7 and q5");
     if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
@@ -237,6 +248,7 @@ int do_verify_correct(const Plan &pl, const void *D, const void *W, void *O, con
                       const ftcnn_policy *pol, ftcnn_report *rep, int32_t cap, void *ws, hipStream_t st) {
     FT_TRY(check_policy(pol));
     if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "verify_correct: null pointer");
+    FT_TRY(check_bias(ck));
     if (!ck->co5 || !ck->so5 || !ck->so6 || !ck->so7 || !ck->q5)
         return fail(FTCNN_E_ARG, "verify needs co5, so5, so6, so7 and q5");
     if (!ck->cd1 || !ck->cd2 || !ck->cw1 || !ck->cw2 || !ck->co6 || !ck->co7)
@@ -279,6 +291,7 @@ int do_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O
                            const ftcnn_policy *pol, ftcnn_report *rep, uint32_t which, void *ws, hipStream_t st) {
     FT_TRY(check_policy(pol));
     if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "verify_correct_sums: null pointer");
+    FT_TRY(check_bias(ck));
     const uint32_t coc = FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7;
     if (which != 0 && which != coc)
         return fail(FTCNN_E_ARG, "verify_correct_sums: which must be 0 or CO5|CO6|CO7 (0x%x)", which);
@@ -295,6 +308,7 @@ int do_correct(const Plan &pl, const void *D, const void *W, void *O, const ftcn
                const ftcnn_policy *pol, ftcnn_report *rep, void *ws, hipStream_t st) {
     FT_TRY(check_policy(pol));
     if (!D || !W || !O || !ck || !rep) return fail(FTCNN_E_ARG, "correct: null pointer");
+    FT_TRY(check_bias(ck));
     if (!ck->cd1 || !ck->cd2 || !ck->cw1 || !ck->cw2 || !ck->co5 || !ck->co6 || !ck->co7)
         return fail(FTCNN_E_ARG, "correct needs cd1, cd2, cw1, cw2, co5, co6 and co7");
     FT_TRY(check_ws(pl, ws));
@@ -386,6 +400,20 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
     FT_TRY(do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, nullptr, 0, workspace, stream));
     return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, workspace,
                                   stream);
+}
+
+int ftcnn_conv_fwd_bias(const ftcnn_conv_desc *desc, const void *D, const void *W, const float *bias,
+                        void *O, void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (!D || !W || !O || !bias) return fail(FTCNN_E_ARG, "conv_fwd_bias: null pointer");
+    if (workspace) {
+        FT_TRY(check_ws(pl, workspace));
+        FT_HIP(launch_conv_ws(pl, D, W, O, workspace, stream, bias), "conv_fwd_bias");
+    } else {
+        FT_HIP(launch_conv(pl, D, W, O, stream, bias), "conv_fwd_bias");
+    }
+    return FTCNN_OK;
 }
 
 int ftcnn_conv_fwd_ws(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O, void *workspace,

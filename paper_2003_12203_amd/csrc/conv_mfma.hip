@@ -534,8 +534,11 @@ template <int EPI> struct Epi {
     CocTile co;
     int co_slices;       // Co partial slices this launch writes (recorded in rep->reserved[1])
     typename std::conditional<EPI == 2, FaultList, NoFaults>::type fl;
+    const float *bias;   // NULL, or [M] added to every stored value of filter m (Sec. 5.1)
 };
-template <> struct Epi<0> {};
+template <> struct Epi<0> {
+    const float *bias;
+};
 
 template <typename T> struct Bits;
 template <> struct Bits<float> {
@@ -752,20 +755,49 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     // epilogue: lane owns pixel (lane & 31) of each 32-wide block; register e of
     // block (i, j) is row 8*(e/4) + 4*(lane/32) + e%4 of that block
     const int l32 = lane & 31, h = lane >> 5;
+    // the tile's bias rows (Sec. 5.1), staged in LDS once the main loop is done: read in the store
+    // loops below from LDS, whose wait never holds on the tile's own output stores
+    const bool hb = ep.bias != nullptr;
+    constexpr size_t kBiasOff = EPI == 0 ? 0 : (size_t)WM * 3 * C::TP * sizeof(double);
+    static_assert(kBiasOff + C::TM * sizeof(float) <= C::LDS_BYTES, "bias rows fit LDS");
+    float *bias_s = reinterpret_cast<float *>(smem + kBiasOff);
+    if (hb) {
+        __syncthreads();   // every wave is done with the operand tiles
+        for (int t = tid; t < C::TM; t += C::NT) bias_s[t] = m0 + t < g.M ? ep.bias[m0 + t] : 0.0f;
+        __syncthreads();
+    }
     if constexpr (EPI == 0) {
+        if (!hb) {
 #pragma unroll
-        for (int j = 0; j < FP; ++j) {
-            const long long pgo = p0 + brow0 + j * 32 + l32;
-            if (pgo >= g.P_total) continue;
-            const long long n = pgo / g.EF;
-            const long long ob = n * g.M * (long long)g.EF + (pgo - n * g.EF);
+            for (int j = 0; j < FP; ++j) {
+                const long long pgo = p0 + brow0 + j * 32 + l32;
+                if (pgo >= g.P_total) continue;
+                const long long n = pgo / g.EF;
+                const long long ob = n * g.M * (long long)g.EF + (pgo - n * g.EF);
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
+                for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int m = m0 + arow0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-                    if (m < g.M) Elem<T>::store(O, ob + (long long)m * g.EF, acc[i][j][e]);
-                }
+                    for (int e = 0; e < 16; ++e) {
+                        const int m = m0 + arow0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+                        if (m < g.M) Elem<T>::store(O, ob + (long long)m * g.EF, acc[i][j][e]);
+                    }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < FP; ++j) {
+                const long long pgo = p0 + brow0 + j * 32 + l32;
+                if (pgo >= g.P_total) continue;
+                const long long n = pgo / g.EF;
+                const long long ob = n * g.M * (long long)g.EF + (pgo - n * g.EF);
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int mt_row = arow0 + i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+                        const int m = m0 + mt_row;
+                        if (m < g.M) Elem<T>::store(O, ob + (long long)m * g.EF, acc[i][j][e] + bias_s[mt_row]);
+                    }
+            }
         }
     } else {
         using Bt = Bits<T>;
@@ -806,9 +838,10 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                 const int m = mrow + mo;
                 const bool mok = m < g.M;
                 const double wm = (double)m + wb;
+                const float bm = hb ? bias_s[m - m0] : 0.0f;
 #pragma unroll
                 for (int j = 0; j < FP; ++j) {
-                    const typename Bt::B b = Bt::make(acc[i][j][e]);
+                    const typename Bt::B b = Bt::make(hb ? acc[i][j][e] + bm : acc[i][j][e]);
                     if (cval[j] && mok) {
                         const double v = (double)Bt::value(b);
                         s1[j] += v;
@@ -1022,8 +1055,8 @@ int conv_tile_m(const Geom &g) {
     return with_tile(g, nhwc_layer(g), [](auto t) { return decltype(t)::TM; });
 }
 
-hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st) {
-    const Epi<0> ep{};
+hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st, const float *bias) {
+    const Epi<0> ep{bias};
     return with_tile(pl.g, false, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
@@ -1070,22 +1103,24 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
     double *part = reinterpret_cast<double *>(w + pl.off_sums);
     double *copart = reinterpret_cast<double *>(w + pl.off_copart);
     const double *cw1 = ck ? ck->cw1 : nullptr, *cw2 = ck ? ck->cw2 : nullptr;
+    const float *bias = ck ? ck->bias : nullptr;
     if (nf == 0) {
-        Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}};
+        Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
         return with_tile(pl.g, pl.nhwc, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp); });
     }
-    Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}};
+    Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
     return with_tile(pl.g, pl.nhwc, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp); });
 }
 
-hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st) {
-    if (!pl.nhwc) return launch_conv(pl, D, W, O, st);
+hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st,
+                          const float *bias) {
+    if (!pl.nhwc) return launch_conv(pl, D, W, O, st, bias);
     const hipError_t e = launch_prep(pl, D, W, nullptr, nullptr, ws, st);
     if (e != hipSuccess) return e;
     char *w = static_cast<char *>(ws);
-    const Epi<0> ep{};
+    const Epi<0> ep{bias};
     return with_tile(pl.g, true, [&](auto t) {
         return decltype(t)::run(pl.g, w + pl.off_dt, w + pl.off_wt, O, st, ep, true, w + pl.off_zero);
     });

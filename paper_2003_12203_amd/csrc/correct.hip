@@ -52,7 +52,26 @@ template <typename T> struct Ctx {
     int *fix_n, *fix_m;
     uint32_t *fix_old;
     ftcnn_report *rep;
+    // bias (Sec. 5.1): NULL, or [M] with cb = {sum_m bias[m], sum_m (m + wbase) bias[m]};
+    // wn = sum_n (n + wbase)
+    const float *bias;
+    const double *cb;
+    double wn;
 };
+
+// The bias shares of Table 5 (Sec. 5.1) moved to the checksum side: the checksums stay
+// those of the convolution, and every comparison with a summation of the biased output
+// (or repair from one) uses Co plus the share that the summation carries.
+template <typename T> __device__ inline double bias_of(const Ctx<T> &c, int m) {
+    return c.bias ? (double)c.bias[m] : 0.0;
+}
+template <typename T> __device__ inline void add_bias_shares(const Ctx<T> &c, double (&co)[3]) {
+    if (!c.bias) return;
+    const double b1 = c.cb[0], b2 = c.cb[1];
+    co[0] += (double)c.g.N * b1;   // So5 carries N sum_m bias[m]
+    co[1] += (double)c.g.N * b2;   // So6 carries N sum_m (m + wbase) bias[m]
+    co[2] += c.wn * b1;            // So7 carries sum_n (n + wbase) sum_m bias[m]
+}
 
 __device__ inline double wave_sum(double v) {
 #pragma unroll
@@ -197,7 +216,7 @@ template <typename T> __device__ double element(const Ctx<T> &c, int n, int m, i
                 if (ih < 0 || ih >= g.H || iw < 0 || iw >= g.W) continue;
                 acc = fma(ldo(Dn, ((long long)ch * g.H + ih) * g.W + iw), ldo(Wm, k), acc);
             }
-    return acc;
+    return acc + bias_of(c, m);
 }
 
 // Per filter m at p: Co1 = Cd1 (x) W_m, Co3 = Cd2 (x) W_m, and the
@@ -237,8 +256,12 @@ template <typename T> __device__ void row_arrays(const Ctx<T> &c, int p, int x, 
             s3 = fma((double)(n + c.wb), o, s3);
             q = fma(o, o, q);
         }
+        // So1[m] carries N bias[m] and So3[m] sum_n (n + wbase) bias[m] (Sec. 5.1); co1m keeps the
+        // shifted Co1, so the repairs from it give biased values
+        const double bm = bias_of(c, m);
+        c.co1m[m] += (double)g.N * bm;
         c.d1[m] = c.co1m[m] - s1;
-        c.d3[m] = c.d3[m] - s3;
+        c.d3[m] = c.d3[m] + c.wn * bm - s3;
         c.q1[m] = sqrt(q);
     }
     __syncthreads();
@@ -281,6 +304,11 @@ template <typename T> __device__ void col_arrays(const Ctx<T> &c, int p, int x, 
             s2 += o;
             s4 = fma((double)(m + c.wb), o, s4);
             q = fma(o, o, q);
+        }
+        // So2[n] carries sum_m bias[m] and So4[n] sum_m (m + wbase) bias[m] (Sec. 5.1)
+        if (c.bias) {
+            c.co2n[n] += c.cb[0];
+            c.d4[n] += c.cb[1];
         }
         c.d2[n] = c.co2n[n] - s2;
         c.d4[n] = c.d4[n] - s4;
@@ -413,7 +441,7 @@ __device__ bool scheme_coc(const Ctx<T> &c, Sh &sh, int p, int x, int y, const d
                 a[0] = fma(ldo(Dn, ((long long)ch * c.g.H + ih) * c.g.W + iw), ldo(Wm, k), a[0]);
         }
         bsum<1>(a, sh);
-        v = a[0];
+        v = a[0] + bias_of(c, j);
     } else {
         v = co[0] - e[0];
     }
@@ -578,6 +606,7 @@ template <typename T> __device__ void resolve(const Ctx<T> &c, Sh &sh, int p, co
     if (agree) {  // an inconsistent pattern among Co5/Co6/Co7: suspect the checksums
         double f[3];
         fresh_coc(c, x, y, sh, f);
+        add_bias_shares(c, f);
         co[0] = f[0]; co[1] = f[1]; co[2] = f[2];
         if (!is_bad(co[0] - s[0], s[3], c.scale) && !is_bad(co[1] - s[1], s[4], c.scale) &&
             !is_bad(co[2] - s[2], s[5], c.scale)) {
@@ -642,7 +671,8 @@ __global__ __launch_bounds__(kThreads) void correct_kernel(Ctx<T> c, const int *
         const int cnt = sh.nlist;
         for (int i = 0; i < cnt; ++i) {
             const int p = sh.list[i];
-            const double co[3] = {c.co5g[p], c.co6g[p], c.co7g[p]};
+            double co[3] = {c.co5g[p], c.co6g[p], c.co7g[p]};
+            add_bias_shares(c, co);
             resolve(c, sh, p, co);
         }
         __syncthreads();
@@ -805,12 +835,15 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
         so6[p] = b;
         so7[p] = cc;
         q5[p] = q;
-        flag = is_bad(c5 - a, q, c.scale) ? 1 : 0;
+        // the checksums as the summations of the biased output see them (Sec. 5.1)
+        double cs[3] = {c5, c6, c7};
+        add_bias_shares(c, cs);
+        flag = is_bad(cs[0] - a, q, c.scale) ? 1 : 0;
         flags[p] = flag;
         sh.flagbuf[slot] = flag;
-        sh.colist[slot][0] = c5;
-        sh.colist[slot][1] = c6;
-        sh.colist[slot][2] = c7;
+        sh.colist[slot][0] = cs[0];
+        sh.colist[slot][1] = cs[1];
+        sh.colist[slot][2] = cs[2];
     }
     const int cnt = __syncthreads_count(flag);
     if (cnt == 0) return;
@@ -866,6 +899,9 @@ Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftc
     c.clc_on = pol.clc_on;
     c.recompute = pol.repair == FTCNN_REPAIR_RECOMPUTE;
     c.rep = rep;
+    c.bias = ck.bias;
+    c.cb = ck.bias ? ck.cb : nullptr;
+    c.wn = (double)pl.g.N * (double)pl.g.wbase + (double)pl.g.N * ((double)pl.g.N - 1.0) / 2.0;
     return c;
 }
 
@@ -924,6 +960,9 @@ hipError_t run(const Plan &pl, const void *D, const void *W, void *O, const ftcn
     c.clc_on = pol.clc_on;
     c.recompute = pol.repair == FTCNN_REPAIR_RECOMPUTE;
     c.rep = rep;
+    c.bias = ck.bias;
+    c.cb = ck.bias ? ck.cb : nullptr;
+    c.wn = (double)pl.g.N * (double)pl.g.wbase + (double)pl.g.N * ((double)pl.g.N - 1.0) / 2.0;
     char *w = static_cast<char *>(ws);
     const int *flags = reinterpret_cast<const int *>(w + pl.off_flags);
     double *scratch = reinterpret_cast<double *>(w + pl.off_corr);

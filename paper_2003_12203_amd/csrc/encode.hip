@@ -124,7 +124,39 @@ hipError_t run(const T *X, long long rows, long long cols, int splits, int wbase
     return hipGetLastError();
 }
 
+// The bias sums of Sec. 5.1, c1 = sum_m b[m] and c2 = sum_m (m + wbase) b[m]: one
+// workgroup, strided per-thread sums added by a fixed tree (deterministic).
+__global__ __launch_bounds__(kThreads) void bias_sums_kernel(const float *__restrict__ b, int M, int wbase,
+                                                             double *c1, double *c2) {
+    __shared__ double red[2][kThreads];
+    const int t = threadIdx.x;
+    double s1 = 0.0, s2 = 0.0;
+    for (int m = t; m < M; m += kThreads) {
+        const double v = (double)b[m];
+        s1 += v;
+        s2 = fma((double)(m + wbase), v, s2);
+    }
+    red[0][t] = s1;
+    red[1][t] = s2;
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        __syncthreads();
+        if (t < h) {
+            red[0][t] += red[0][t + h];
+            red[1][t] += red[1][t + h];
+        }
+    }
+    if (t == 0) {
+        *c1 = red[0][0];
+        *c2 = red[1][0];
+    }
+}
+
 }  // namespace
+
+hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, double *c2, hipStream_t st) {
+    bias_sums_kernel<<<1, kThreads, 0, st>>>(bias, pl.g.M, pl.g.wbase, c1, c2);
+    return hipGetLastError();
+}
 
 hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, double *c2,
                          void *ws, hipStream_t st) {

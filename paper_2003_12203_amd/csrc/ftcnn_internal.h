@@ -143,7 +143,11 @@ KernelEvents &kernel_events();
 
 hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, double *c2,
                          void *ws, hipStream_t st);
-hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st);
+// bias: NULL, or fp32 [M] added to every O[n][m] before rounding (Sec. 5.1).
+hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st,
+                       const float *bias = nullptr);
+// c1 = sum_m bias[m], c2 = sum_m (m + wbase) bias[m] (Sec. 5.1), one double each.
+hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, double *c2, hipStream_t st);
 // The convolution with the CoC-D summations in its epilogue: every tile also
 // writes its (So5, So6, So7, sum of squares) partials for the pixels it owns to
 // the workspace (pl.sum_splits slices, layout of the verification partials) and
@@ -185,7 +189,8 @@ hipError_t launch_prep(const Plan &pl, const void *D, const void *W, double *cd1
                        hipStream_t st);
 // The convolution alone through the path ftcnn_conv_fwd_sums takes (channels-last
 // copies for pl.nhwc layers): O bitwise equal to that of launch_conv_sums.
-hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st);
+hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st,
+                          const float *bias = nullptr);
 hipError_t launch_checksum_conv(const Plan &pl, uint32_t which, const void *D, const void *W,
                                 const ftcnn_checksums &ck, hipStream_t st);
 hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &ck,

@@ -140,7 +140,7 @@ __global__ __launch_bounds__(kThreads) void verify_final(Geom g, int splits, con
                                                          const double *__restrict__ co5, double *so5,
                                                          double *so6, double *so7, double *q5,
                                                          int *__restrict__ flags, double scale,
-                                                         ftcnn_report *rep) {
+                                                         const double *__restrict__ cb, ftcnn_report *rep) {
     const int lane = threadIdx.x % TPP;
     const int p = blockIdx.x * (kThreads / TPP) + threadIdx.x / TPP;
     double a = 0.0, b = 0.0, c = 0.0, d = 0.0;
@@ -167,7 +167,9 @@ __global__ __launch_bounds__(kThreads) void verify_final(Geom g, int splits, con
         so6[p] = b;
         so7[p] = c;
         q5[p] = q;
-        flag = is_bad(co5[p] - a, q, scale) ? 1 : 0;
+        // with a bias, So5 less its share N * sum_m bias[m] (Sec. 5.1) is what Co5 predicts
+        const double share = cb ? (double)g.N * cb[0] : 0.0;
+        flag = is_bad(co5[p] - (a - share), q, scale) ? 1 : 0;
         flags[p] = flag;
     }
     const int cnt = __syncthreads_count(flag);
@@ -218,7 +220,7 @@ hipError_t launch_verify(const Plan &pl, const void *O, const ftcnn_checksums &c
     const int sp = pl.ver_splits;
 #define FINAL(TPP)                                                                                     \
     verify_final<TPP><<<(unsigned)((g.EF + kThreads / TPP - 1) / (kThreads / TPP)), kThreads, 0, st>>>( \
-        g, sp, part, ck.co5, ck.so5, ck.so6, ck.so7, ck.q5, flags, scale, rep)
+        g, sp, part, ck.co5, ck.so5, ck.so6, ck.so7, ck.q5, flags, scale, ck.bias ? ck.cb : nullptr, rep)
     if (sp <= 1) FINAL(1);
     else if (sp <= 4) FINAL(4);
     else if (sp <= 16) FINAL(16);

@@ -29,13 +29,22 @@ def test_library_exports_every_declared_symbol():
 
 def test_struct_sizes_match_header_layout():
     assert C.sizeof(_lib.ConvDesc) == 12 * 4
-    assert C.sizeof(_lib.Checksums) == 15 * 8
+    assert C.sizeof(_lib.Checksums) == 17 * 8   # 15 checksum arrays, the bias and its sums
     assert C.sizeof(_lib.ReportHeader) == 14 * 4
     assert C.sizeof(_lib.Fix) == 5 * 4
     assert C.sizeof(_lib.Policy) == 4 * 4 + 2 * 8
     assert C.sizeof(_lib.Fault) == 6 * 4 + 8
     assert ft.report_bytes(0) == C.sizeof(_lib.ReportHeader)
     assert ft.report_bytes(7) == C.sizeof(_lib.ReportHeader) + 7 * C.sizeof(_lib.Fix)
+
+
+def test_checksums_field_order_matches_header():
+    import re
+    text = open(os.path.join(ROOT, "include", "ftcnn.h")).read()
+    body = text[text.index("typedef struct {\n    double *cd1"):text.index("} ftcnn_checksums;")]
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = re.findall(r"\*\s*(\w+)", body)
+    assert names == [f[0] for f in _lib.Checksums._fields_]
 
 
 @pytest.mark.parametrize("h,r,u,p,e", [(227, 11, 4, 0, 55), (224, 7, 2, 3, 112), (56, 1, 2, 0, 28),
