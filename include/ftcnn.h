@@ -174,6 +174,15 @@ const char *ftcnn_last_error(void);
 int ftcnn_encode(const ftcnn_conv_desc *desc, int32_t which, const void *X,
                  double *c1, double *c2, void *workspace, hipStream_t stream);
 
+/* Weights in memory (Sec. 4.1.2): a soft error in W shows as a difference between Cw1
+ * re-encoded from the current W and cw1 encoded before the application (ftcnn_encode,
+ * which = 1); the remedy is to reload W.  The re-encode runs the same deterministic kernels,
+ * so intact weights reproduce cw1 bit for bit and the comparison is exact.  *mismatches
+ * (device int32) receives the number of columns (c, r, s) whose sums differ: 0 when W is
+ * intact.  Uses the workspace. */
+int ftcnn_check_weights(const ftcnn_conv_desc *desc, const void *W, const double *cw1, int32_t *mismatches,
+                        void *workspace, hipStream_t stream);
+
 /* Eq. (1) without bias, with zero padding: O[n][m][x][y] = sum_{k,i,j}
  * D[n][k][Ux+i-P][Uy+j-P] W[m][k][i][j].  Implicit GEMM on the matrix cores,
  * fp32 accumulation, O rounded to the layer dtype (nearest even). */

@@ -191,6 +191,14 @@ def col_checksums(ck: Checksums, D: np.ndarray, stride: int, pad: int):
     return (checksum_conv(D, ck.cw1, stride, pad)[:, 0], checksum_conv(D, ck.cw2, stride, pad)[:, 0])
 
 
+def check_weights(W: np.ndarray, cw1: np.ndarray, wbase: int = 0) -> int:
+    """Sec. 4.1.2: the columns (c, r, s) of W whose sum over the filters no longer equals the Cw1
+    encoded before the application (a soft error in the weights in memory; the remedy is to
+    reload W).  The same encode reproduces an intact column bit for bit."""
+    fresh, _ = encode(W, wbase)
+    return int(np.count_nonzero(fresh != cw1))
+
+
 @dataclasses.dataclass
 class BiasTerms:
     """The bias shares of the output summations (Sec. 5.1, Table 5), precomputed from Bias[m]:

@@ -113,6 +113,11 @@ def verify_correct(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
            "ftcnn_verify_correct")
 
 
+def check_weights(desc, W, cw1, mismatches: torch.Tensor, workspace, stream=None) -> None:
+    _check(lib().ftcnn_check_weights(C.byref(desc), _ptr(W), _ptr(cw1), _ptr(mismatches), _ptr(workspace),
+                                     _stream(stream)), "ftcnn_check_weights")
+
+
 def conv_fwd_bias(desc, D, W, bias, O, workspace=None, stream=None) -> None:
     _check(lib().ftcnn_conv_fwd_bias(C.byref(desc), _ptr(D), _ptr(W), _ptr(bias), _ptr(O), _ptr(workspace),
                                      _stream(stream)), "ftcnn_conv_fwd_bias")
@@ -274,6 +279,13 @@ class Layer:
     # the entry points on this layer's buffers
     def encode_weights(self, W, stream=None):
         encode(self.desc, 1, W, self.buf["cw1"], self.buf["cw2"], self.workspace, stream)
+
+    def check_weights(self, W, stream=None) -> int:
+        """Columns of W whose sum no longer equals the Cw1 encoded at set-up (Sec. 4.1.2); 0 when
+        W is intact, otherwise W should be reloaded.  Synchronizes."""
+        out = torch.zeros(1, dtype=torch.int32, device=self.buf["cw1"].device)
+        check_weights(self.desc, W, self.buf["cw1"], out, self.workspace, stream)
+        return int(out.item())
 
     def encode_input(self, D, stream=None):
         encode(self.desc, 0, D, self.buf["cd1"], self.buf["cd2"], self.workspace, stream)

@@ -56,7 +56,7 @@ class Fault(C.Structure):
 EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ftcnn_last_error",
            "ftcnn_encode", "ftcnn_conv_fwd", "ftcnn_checksum_conv", "ftcnn_verify", "ftcnn_correct",
            "ftcnn_verify_correct", "ftcnn_conv_fwd_ws", "ftcnn_conv_fwd_sums", "ftcnn_verify_correct_sums", "ftcnn_protected_conv",
-           "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias")
+           "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias", "ftcnn_check_weights")
 
 _lib = None
 
@@ -92,6 +92,8 @@ def load(path: str = LIB_PATH):
     L.ftcnn_verify_correct.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp, C.c_int32,
                                        _dp, _dp]
     L.ftcnn_verify_correct.restype = C.c_int
+    L.ftcnn_check_weights.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp]
+    L.ftcnn_check_weights.restype = C.c_int
     L.ftcnn_conv_fwd_bias.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp, _dp]
     L.ftcnn_conv_fwd_bias.restype = C.c_int
     L.ftcnn_conv_fwd_ws.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp]

@@ -152,6 +152,8 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     off += pl->co_in_conv ? align256(3ull * pl->co.groups * pl->prep_ns * EF * sizeof(double)) : 0;
     pl->off_corr = off;
     off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
+    pl->off_wchk = off;   // Cw1, Cw2 re-encoded by ftcnn_check_weights
+    off += align256(2 * sizeof(double) * (size_t)K);
     pl->bytes = off;
     return FTCNN_OK;
 }
@@ -400,6 +402,16 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
     FT_TRY(do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, nullptr, 0, workspace, stream));
     return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, workspace,
                                   stream);
+}
+
+int ftcnn_check_weights(const ftcnn_conv_desc *desc, const void *W, const double *cw1, int32_t *mismatches,
+                        void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (!W || !cw1 || !mismatches) return fail(FTCNN_E_ARG, "check_weights: null pointer");
+    FT_TRY(check_ws(pl, workspace));
+    FT_HIP(launch_check_weights(pl, W, cw1, mismatches, workspace, stream), "check_weights");
+    return FTCNN_OK;
 }
 
 int ftcnn_conv_fwd_bias(const ftcnn_conv_desc *desc, const void *D, const void *W, const float *bias,

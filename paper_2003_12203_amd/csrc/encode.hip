@@ -151,7 +151,34 @@ __global__ __launch_bounds__(kThreads) void bias_sums_kernel(const float *__rest
     }
 }
 
+// Columns whose re-encoded Cw1 differs bitwise from the stored one: one workgroup, strided
+// per-thread counts added by a fixed tree.
+__global__ __launch_bounds__(kThreads) void count_mismatch_kernel(const double *__restrict__ fresh,
+                                                                  const double *__restrict__ cw1, long long K,
+                                                                  int32_t *out) {
+    __shared__ int red[kThreads];
+    const int t = threadIdx.x;
+    int c = 0;
+    for (long long k = t; k < K; k += kThreads)
+        c += __double_as_longlong(fresh[k]) != __double_as_longlong(cw1[k]) ? 1 : 0;
+    red[t] = c;
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        __syncthreads();
+        if (t < h) red[t] += red[t + h];
+    }
+    if (t == 0) *out = red[0];
+}
+
 }  // namespace
+
+hipError_t launch_check_weights(const Plan &pl, const void *W, const double *cw1, int32_t *mismatches, void *ws,
+                                hipStream_t st) {
+    double *fresh = reinterpret_cast<double *>(static_cast<char *>(ws) + pl.off_wchk);
+    const hipError_t e = launch_encode(pl, 1, W, fresh, fresh + pl.g.K, ws, st);
+    if (e != hipSuccess) return e;
+    count_mismatch_kernel<<<1, kThreads, 0, st>>>(fresh, cw1, pl.g.K, mismatches);
+    return hipGetLastError();
+}
 
 hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, double *c2, hipStream_t st) {
     bias_sums_kernel<<<1, kThreads, 0, st>>>(bias, pl.g.M, pl.g.wbase, c1, c2);

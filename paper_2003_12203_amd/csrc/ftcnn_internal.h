@@ -56,7 +56,8 @@ struct Plan {
     int prep_ns;                      // image ranges of the encode fused into the channels-last copy
     bool co_in_conv;                  // Co5..Co7 partials computed by workgroups of the convolution launch
     CocTile co;                       // their tiling (co_in_conv)
-    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, off_zero, bytes;
+    size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, off_zero,
+        off_wchk, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
 
@@ -146,6 +147,10 @@ hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, d
 // bias: NULL, or fp32 [M] added to every O[n][m] before rounding (Sec. 5.1).
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st,
                        const float *bias = nullptr);
+// Re-encode Cw1, Cw2 of W into the workspace (pl.off_wchk) and count the columns whose Cw1
+// differs bitwise from cw1 into *mismatches (Sec. 4.1.2).
+hipError_t launch_check_weights(const Plan &pl, const void *W, const double *cw1, int32_t *mismatches, void *ws,
+                                hipStream_t st);
 // c1 = sum_m bias[m], c2 = sum_m (m + wbase) bias[m] (Sec. 5.1), one double each.
 hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, double *c2, hipStream_t st);
 // The convolution with the CoC-D summations in its epilogue: every tile also

@@ -8,6 +8,8 @@
 * The whole workflow with a bias: a clean layer is not flagged, and each fault pattern is
   resolved by the same scheme as without a bias, back to the biased clean output exactly.
 * A zero bias changes nothing.
+* The weight-memory check (Sec. 4.1.2) counts exactly the columns of W corrupted after Cw1
+  was encoded.
 """
 import numpy as np
 import pytest
@@ -86,3 +88,19 @@ def test_zero_bias_is_no_bias():
     b = wf.protect(D, W, 1, 1, "f32", faults=faults, bias=np.zeros(spec.m))
     np.testing.assert_array_equal(a.O, b.O)
     assert a.report.fixes == b.report.fixes
+
+
+@pytest.mark.parametrize("cols", [0, 1, 3])
+def test_weight_check_counts_corrupted_columns(cols):
+    """Sec. 4.1.2: corrupting elements of W after Cw1 is encoded shows in exactly the columns hit."""
+    spec, _, W, _ = _int_layer(m=9, seed=37)
+    cw1, _ = wf.encode(W, 0)
+    W2 = W.copy()
+    g = np.random.default_rng([12203, 71, cols])
+    flat = g.choice(W.shape[1] * W.shape[2] * W.shape[3], size=cols, replace=False)
+    for k in flat:
+        c, rs = divmod(int(k), W.shape[2] * W.shape[3])
+        r, s = divmod(rs, W.shape[3])
+        W2[g.integers(0, W.shape[0]), c, r, s] += 0.5      # exact in float64
+    assert wf.check_weights(W2, cw1) == cols
+    assert wf.check_weights(W, cw1) == 0
