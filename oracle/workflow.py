@@ -34,6 +34,10 @@ Readings where the paper is silent (all shared with the HIP library):
   fault with no repair; otherwise the chain continues with the fresh ones;
 * positions left unresolved trigger a recomputation of the whole layer
   (Sec. 4.1.1);
+* with G groups (Sec. 5.2) filter block m convolves only with channel group
+  m // (M/G) of every feature-map block; Cd stays, Cw1/Cw2 are the per-group filter
+  sums laid side by side over the channels (m counted over all filters in Cw2), and
+  the tolerance's K is the per-output dot length (Ch/G)*R*S;
 * with a bias (Sec. 5.1) the output is eq. (1) plus Bias[m], the checksums stay
   those of the convolution, and every summation has the bias share of Table 5
   subtracted before it is compared or used in a repair (with the paper's index
@@ -154,6 +158,27 @@ def encode(X: np.ndarray, wbase: int = 0) -> Tuple[np.ndarray, np.ndarray]:
     return core.block_sums(X, float(wbase))
 
 
+def encode_weights(W: np.ndarray, groups: int = 1, wbase: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """Cw1, Cw2 of Sec. 3.2; with G groups (Sec. 5.2) the sums over the filters of each group,
+    laid side by side over the channels ([Ch][R][S] for W [M][Ch/G][R][S]), the weight of
+    filter m being m + wbase with m counted over all filters."""
+    if groups == 1:
+        return encode(W, wbase)
+    Mg = W.shape[0] // groups
+    parts = [encode(W[g * Mg:(g + 1) * Mg], wbase + g * Mg) for g in range(groups)]
+    return np.concatenate([a for a, _ in parts], axis=0), np.concatenate([b for _, b in parts], axis=0)
+
+
+def grouped_conv(D: np.ndarray, W: np.ndarray, groups: int, stride: int, pad: int) -> np.ndarray:
+    """Eq. (1) with G groups (Sec. 5.2): filter block m convolves with channel group m // (M/G)
+    of every feature-map block only."""
+    if groups == 1:
+        return core.conv(D, W, stride, pad)
+    Cg, Mg = D.shape[1] // groups, W.shape[0] // groups
+    return np.concatenate([core.conv(D[:, g * Cg:(g + 1) * Cg], W[g * Mg:(g + 1) * Mg], stride, pad)
+                           for g in range(groups)], axis=1)
+
+
 @dataclasses.dataclass
 class Checksums:
     cd1: np.ndarray
@@ -181,9 +206,16 @@ def coc_checksums(ck: Checksums, stride: int, pad: int) -> None:
     ck.co7 = checksum_conv(ck.cd2, ck.cw1, stride, pad)[0, 0]
 
 
-def row_checksums(ck: Checksums, W: np.ndarray, stride: int, pad: int):
-    """Co1 = Cd1 (x) W and Co3 = Cd2 (x) W (Sec. 3.2), each [M][E][F]."""
-    return (checksum_conv(ck.cd1, W, stride, pad)[0], checksum_conv(ck.cd2, W, stride, pad)[0])
+def row_checksums(ck: Checksums, W: np.ndarray, stride: int, pad: int, groups: int = 1):
+    """Co1 = Cd1 (x) W and Co3 = Cd2 (x) W (Sec. 3.2), each [M][E][F]; with G groups each
+    filter block meets its own channel group of Cd1, Cd2 (Sec. 5.2)."""
+    if groups == 1:
+        return (checksum_conv(ck.cd1, W, stride, pad)[0], checksum_conv(ck.cd2, W, stride, pad)[0])
+    Cg, Mg = ck.cd1.shape[0] // groups, W.shape[0] // groups
+    rows = [(checksum_conv(ck.cd1[g * Cg:(g + 1) * Cg], W[g * Mg:(g + 1) * Mg], stride, pad)[0],
+             checksum_conv(ck.cd2[g * Cg:(g + 1) * Cg], W[g * Mg:(g + 1) * Mg], stride, pad)[0])
+            for g in range(groups)]
+    return np.concatenate([a for a, _ in rows], axis=0), np.concatenate([b for _, b in rows], axis=0)
 
 
 def col_checksums(ck: Checksums, D: np.ndarray, stride: int, pad: int):
@@ -191,11 +223,11 @@ def col_checksums(ck: Checksums, D: np.ndarray, stride: int, pad: int):
     return (checksum_conv(D, ck.cw1, stride, pad)[:, 0], checksum_conv(D, ck.cw2, stride, pad)[:, 0])
 
 
-def check_weights(W: np.ndarray, cw1: np.ndarray, wbase: int = 0) -> int:
+def check_weights(W: np.ndarray, cw1: np.ndarray, wbase: int = 0, groups: int = 1) -> int:
     """Sec. 4.1.2: the columns (c, r, s) of W whose sum over the filters no longer equals the Cw1
     encoded before the application (a soft error in the weights in memory; the remedy is to
     reload W).  The same encode reproduces an intact column bit for bit."""
-    fresh, _ = encode(W, wbase)
+    fresh, _ = encode_weights(W, groups, wbase)
     return int(np.count_nonzero(fresh != cw1))
 
 
@@ -279,8 +311,9 @@ def verify(O: np.ndarray, co5: np.ndarray, K: int, dtype: str, policy: Policy,
 # ----------------------------------------------------------------------------
 
 class _Layer:
-    def __init__(self, O, D, W, ck, stride, pad, dtype, policy, bt=None):
+    def __init__(self, O, D, W, ck, stride, pad, dtype, policy, bt=None, groups=1):
         self.O, self.D, self.W, self.ck = O, D, W, ck
+        self.G = groups
         self.stride, self.pad, self.dtype, self.pol = stride, pad, dtype, policy
         self.N, self.M, self.E, self.F = O.shape
         self.K = W.shape[1] * W.shape[2] * W.shape[3]
@@ -293,7 +326,7 @@ class _Layer:
     # lazily computed per-layer checksum arrays (the paper computes them on demand, Sec. 4.3)
     def rows(self):
         if self._rows is None:
-            self._rows = row_checksums(self.ck, self.W, self.stride, self.pad)
+            self._rows = row_checksums(self.ck, self.W, self.stride, self.pad, self.G)
         return self._rows
 
     def cols(self):
@@ -305,7 +338,7 @@ class _Layer:
         """Co5..Co7 from input checksums re-encoded out of the current D and W."""
         if self._fresh is None:
             cd1, cd2 = encode(self.D, self.pol.wbase)
-            cw1, cw2 = encode(self.W, self.pol.wbase)
+            cw1, cw2 = encode_weights(self.W, self.G, self.pol.wbase)
             f = Checksums(cd1, cd2, cw1, cw2)
             coc_checksums(f, self.stride, self.pad)
             self._fresh = (f.co5, f.co6, f.co7)
@@ -340,8 +373,10 @@ class _Layer:
         return int(i)
 
     def element(self, n, m, x, y):
-        """Eq. (1) for one element, plus its bias (the RECOMPUTE repair option)."""
-        return core.conv_points(self.D, self.W, self.stride, self.pad,
+        """Eq. (1) for one element (over the filter's channel group), plus its bias (the RECOMPUTE
+        repair option)."""
+        Cg, g = self.D.shape[1] // self.G, m // (self.M // self.G)
+        return core.conv_points(self.D[:, g * Cg:(g + 1) * Cg], self.W, self.stride, self.pad,
                                 np.array([[n, m, x, y]], dtype=np.int32))[0] + self.bt.bias[m]
 
     def excl_row(self, co1m, m, i, x, y):
@@ -515,7 +550,8 @@ class _Layer:
 
 
 def correct(O: np.ndarray, D: np.ndarray, W: np.ndarray, ck: Checksums, flags: np.ndarray,
-            stride: int, pad: int, dtype: str, policy: Policy, bt: Optional[BiasTerms] = None) -> Report:
+            stride: int, pad: int, dtype: str, policy: Policy, bt: Optional[BiasTerms] = None,
+            groups: int = 1) -> Report:
     """Correction module of the multischeme workflow (Sec. 4.3), O repaired in place."""
     rep = Report()
     E, F = O.shape[2:]
@@ -525,7 +561,7 @@ def correct(O: np.ndarray, D: np.ndarray, W: np.ndarray, ck: Checksums, flags: n
     if not rep.detected:
         rep.status = STATUS_CLEAN
         return rep
-    L = _Layer(O, D, W, ck, stride, pad, dtype, policy, bt)
+    L = _Layer(O, D, W, ck, stride, pad, dtype, policy, bt, groups)
     for p in rep.flagged:
         x, y = divmod(p, F)
         scheme, fixes = L.resolve(x, y)
@@ -556,7 +592,7 @@ class LayerResult:
 def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
             policy: Optional[Policy] = None, faults: Sequence[Fault] = (),
             O_in: Optional[np.ndarray] = None, after_encode=None,
-            bias: Optional[np.ndarray] = None) -> LayerResult:
+            bias: Optional[np.ndarray] = None, groups: int = 1) -> LayerResult:
     """One protected layer: encode, convolve, checksum convs, verify, correct, recompute.
 
     ``after_encode(D, W, ck)`` may corrupt copies of D, W or the input
@@ -565,7 +601,8 @@ def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
     ``O_in`` replaces the oracle's own convolution (decision-oracle mode: the
     caller supplies an output, e.g. a faulted one, and the workflow decides on
     it).  ``O_clean`` is always the output of the uncorrupted inputs.  ``bias`` [M] is added
-    to every output block O[n][m] (Sec. 5.1).
+    to every output block O[n][m] (Sec. 5.1).  ``groups`` G > 1: W is [M][Ch/G][R][S] and filter
+    block m convolves with channel group m // (M/G) only (Sec. 5.2).
     """
     policy = policy or Policy()
     D = np.array(D, dtype=np.float64)
@@ -574,10 +611,10 @@ def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
     bt = BiasTerms.make(bias, D.shape[0], W.shape[0], policy.wbase)
 
     def conv_b(D_, W_):
-        return store(core.conv(D_, W_, stride, pad) + bt.bias[None, :, None, None], dtype)
+        return store(grouped_conv(D_, W_, groups, stride, pad) + bt.bias[None, :, None, None], dtype)
 
     O_clean = conv_b(D, W)
-    cw1, cw2 = encode(W, policy.wbase)  # before the application (Sec. 4.2)
+    cw1, cw2 = encode_weights(W, groups, policy.wbase)  # before the application (Sec. 4.2)
     cd1, cd2 = encode(D, policy.wbase)  # before the convolution (Sec. 3.3)
     ck = Checksums(cd1, cd2, cw1, cw2)
     touched = False
@@ -594,7 +631,7 @@ def protect(D: np.ndarray, W: np.ndarray, stride: int, pad: int, dtype: str,
     apply_faults(O, dtype, faults)
     O_faulty = O.copy()
     so5, so6, so7, q5, flags = verify(O, ck.co5, K, dtype, policy, bt)
-    rep = correct(O, D, W, ck, flags, stride, pad, dtype, policy, bt)
+    rep = correct(O, D, W, ck, flags, stride, pad, dtype, policy, bt, groups)
     if rep.status == STATUS_NEEDS_RECOMPUTE:
         O[...] = conv_b(D, W)
         *_, flags2 = verify(O, ck.co5, K, dtype, policy, bt)

@@ -57,8 +57,8 @@ def _swap_co6_co7(ck, stride, pad):
     ck.co6, ck.co7 = ck.co7, ck.co6
 
 
-def _co1_from_cd2(ck, W, stride, pad):
-    co1, co3 = _orig_rows(ck, W, stride, pad)
+def _co1_from_cd2(ck, W, stride, pad, groups=1):
+    co1, co3 = _orig_rows(ck, W, stride, pad, groups)
     return co3, co3
 
 
