@@ -210,13 +210,14 @@ class Layer:
     """Device buffers of one protected layer and the calls that use them."""
 
     def __init__(self, n, ch, h, w, m, r, s, stride=1, pad=0, dtype="f32", wbase=0,
-                 policy: Optional[_lib.Policy] = None, cap_fixes: int = 4096, device="cuda"):
-        self.desc = make_desc(n, ch, h, w, m, r, s, stride, pad, dtype, wbase)
+                 policy: Optional[_lib.Policy] = None, cap_fixes: int = 4096, device="cuda", groups: int = 1):
+        self.desc = make_desc(n, ch, h, w, m, r, s, stride, pad, dtype, wbase, groups)
+        self.groups = groups
         self.dtype = dtype
         self.tdtype = DTYPES[dtype][1]
         self.E, self.F = out_shape(self.desc)
         self.shape_d = (n, ch, h, w)
-        self.shape_w = (m, ch, r, s)
+        self.shape_w = (m, ch // groups, r, s)   # grouped (Sec. 5.2): each filter sees ch / groups channels
         self.shape_o = (n, m, self.E, self.F)
         self.policy = policy or make_policy()
         self.cap = cap_fixes
@@ -291,7 +292,9 @@ class Layer:
         encode(self.desc, 0, D, self.buf["cd1"], self.buf["cd2"], self.workspace, stream)
 
     def conv(self, D, W, O, stream=None):
-        if self.bias is not None:
+        if self.groups > 1:   # grouped layers run on the expansion of W in the workspace
+            self.conv_ws(D, W, O, stream)
+        elif self.bias is not None:
             conv_fwd_bias(self.desc, D, W, self.bias, O, None, stream)
         else:
             conv_fwd(self.desc, D, W, O, stream)

@@ -40,7 +40,8 @@ int row_splits(long long rows, long long col_blocks, long long target_blocks, lo
 
 int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     if (!d) return fail(FTCNN_E_ARG, "null descriptor");
-    if (d->groups != 1) return fail(FTCNN_E_UNSUPPORTED, "groups = %d (only 1 is supported)", d->groups);
+    if (d->groups < 1 || d->ch % d->groups != 0 || d->m % d->groups != 0)
+        return fail(FTCNN_E_SHAPE, "groups = %d must divide ch = %d and m = %d", d->groups, d->ch, d->m);
     if (d->dtype != FTCNN_F32 && d->dtype != FTCNN_BF16) return fail(FTCNN_E_DTYPE, "dtype %d", d->dtype);
     if (d->wbase != 0 && d->wbase != 1) return fail(FTCNN_E_ARG, "wbase %d (0 or 1)", d->wbase);
     if (d->n < 1 || d->ch < 1 || d->h < 1 || d->w < 1 || d->m < 1 || d->r < 1 || d->s < 1 ||
@@ -66,6 +67,10 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     g.P_total = (long long)g.N * EF;
     g.dtype = d->dtype;
     g.wbase = d->wbase;
+    g.G = d->groups;
+    g.Cg = d->ch / d->groups;
+    g.Mg = d->m / d->groups;
+    g.Kg = g.Cg * d->r * d->s;
 
     const int vec = g.dtype == FTCNN_F32 ? 4 : 8;
     // input checksums
@@ -154,6 +159,8 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
     pl->off_wchk = off;   // Cw1, Cw2 re-encoded by ftcnn_check_weights
     off += align256(2 * sizeof(double) * (size_t)K);
+    pl->off_wfull = off;  // grouped layers: the block-diagonal expansion of W
+    off += g.G > 1 ? align256((size_t)g.M * K * es) : 0;
     pl->bytes = off;
     return FTCNN_OK;
 }
@@ -176,6 +183,17 @@ int check_ws(const Plan &pl, const void *ws) {
         if (_e != hipSuccess) return hip_fail(_e, where); \
     } while (0)
 
+// The weights the convolution and the weight encode run on: W itself, or on grouped layers its
+// block-diagonal expansion in the workspace (which those layers therefore always need).
+int weights_for_conv(const Plan &pl, const void *W, void *ws, hipStream_t st, const void **out) {
+    if (pl.g.G > 1) FT_TRY(check_ws(pl, ws));
+    hipError_t e;
+    *out = dense_weights(pl, W, ws, st, &e);
+    FT_HIP(e, "grouped weights");
+    return FTCNN_OK;
+}
+
+
 int check_policy(const ftcnn_policy *p) {
     if (!p) return fail(FTCNN_E_ARG, "null policy");
     if (!(p->kappa > 0.0) || !(p->eta >= 0.0 && p->eta < 0.5))
@@ -194,12 +212,15 @@ int do_encode(const Plan &pl, int which, const void *X, double *c1, double *c2, 
     }
     const int splits = which == 0 ? pl.enc_splits_d : pl.enc_splits_w;
     if (splits > 1) FT_TRY(check_ws(pl, ws));
+    if (which == 1) FT_TRY(weights_for_conv(pl, X, ws, st, &X));   // grouped: Sec. 5.2's Cw1, Cw2
     FT_HIP(launch_encode(pl, which, X, c1, c2, ws, st), "encode");
     return FTCNN_OK;
 }
 
 int do_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st) {
     if (!D || !W || !O) return fail(FTCNN_E_ARG, "conv_fwd: null pointer");
+    if (pl.g.G > 1)
+        return fail(FTCNN_E_UNSUPPORTED, "conv_fwd: grouped layers run through ftcnn_conv_fwd_ws (W is expanded in the workspace)");
     FT_HIP(launch_conv(pl, D, W, O, st), "conv_fwd");
     return FTCNN_OK;
 }
@@ -220,6 +241,8 @@ int do_cksum(const Plan &pl, uint32_t which, const void *D, const void *W, const
         return fail(FTCNN_E_ARG, "Co1/Co3 need W, cd1 and cd2");
     if ((which & (FTCNN_CO2 | FTCNN_CO4)) && (!D || !ck->cw1 || !ck->cw2))
         return fail(FTCNN_E_ARG, "Co2/Co4 need D, cw1 and cw2");
+    if ((which & (FTCNN_CO1 | FTCNN_CO3)) && pl.g.G > 1)
+        return fail(FTCNN_E_UNSUPPORTED, "Co1/Co3 of a grouped layer: the correction computes them where flagged");
     if (((which & FTCNN_CO1) && !ck->co1) || ((which & FTCNN_CO3) && !ck->co3) ||
         ((which & FTCNN_CO2) && !ck->co2) || ((which & FTCNN_CO4) && !ck->co4))
         return fail(FTCNN_E_ARG, "checksum_conv: null output array");
@@ -285,6 +308,7 @@ int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ft
         return fail(FTCNN_E_ARG, "conv_fwd_sums: cw1 and cw2 go together");
     FT_TRY(check_faults(pl.g, faults, nf, "conv_fwd_sums"));
     FT_TRY(check_ws(pl, ws));
+    FT_TRY(weights_for_conv(pl, W, ws, st, &W));
     FT_HIP(launch_conv_sums(pl, D, W, O, ck, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
     return FTCNN_OK;
 }
@@ -410,6 +434,7 @@ int ftcnn_check_weights(const ftcnn_conv_desc *desc, const void *W, const double
     FT_TRY(make_plan(desc, &pl));
     if (!W || !cw1 || !mismatches) return fail(FTCNN_E_ARG, "check_weights: null pointer");
     FT_TRY(check_ws(pl, workspace));
+    FT_TRY(weights_for_conv(pl, W, workspace, stream, &W));
     FT_HIP(launch_check_weights(pl, W, cw1, mismatches, workspace, stream), "check_weights");
     return FTCNN_OK;
 }
@@ -421,8 +446,10 @@ int ftcnn_conv_fwd_bias(const ftcnn_conv_desc *desc, const void *D, const void *
     if (!D || !W || !O || !bias) return fail(FTCNN_E_ARG, "conv_fwd_bias: null pointer");
     if (workspace) {
         FT_TRY(check_ws(pl, workspace));
+        FT_TRY(weights_for_conv(pl, W, workspace, stream, &W));
         FT_HIP(launch_conv_ws(pl, D, W, O, workspace, stream, bias), "conv_fwd_bias");
     } else {
+        if (pl.g.G > 1) return fail(FTCNN_E_UNSUPPORTED, "conv_fwd_bias: a grouped layer needs the workspace");
         FT_HIP(launch_conv(pl, D, W, O, stream, bias), "conv_fwd_bias");
     }
     return FTCNN_OK;
@@ -434,6 +461,7 @@ int ftcnn_conv_fwd_ws(const ftcnn_conv_desc *desc, const void *D, const void *W,
     FT_TRY(make_plan(desc, &pl));
     if (!D || !W || !O) return fail(FTCNN_E_ARG, "conv_fwd_ws: null pointer");
     FT_TRY(check_ws(pl, workspace));
+    FT_TRY(weights_for_conv(pl, W, workspace, stream, &W));
     FT_HIP(launch_conv_ws(pl, D, W, O, workspace, stream), "conv_fwd_ws");
     return FTCNN_OK;
 }

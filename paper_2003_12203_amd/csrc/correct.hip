@@ -202,14 +202,15 @@ template <typename T> __device__ void stage_offsets(const Ctx<T> &c, int x, int 
     }
 }
 
-// Eq. (1) for one element, serially in k order (the RECOMPUTE repair).
+// Eq. (1) for one element, serially in k order (the RECOMPUTE repair); on a grouped layer over
+// the filter's channel group (Sec. 5.2), W being [M][Cg][R][S].
 template <typename T> __device__ double element(const Ctx<T> &c, int n, int m, int x, int y) {
     const Geom &g = c.g;
-    const T *Dn = c.D + (long long)n * g.CHW;
-    const T *Wm = c.W + (long long)m * g.K;
+    const T *Dn = c.D + (long long)n * g.CHW + (long long)group_first_channel(g, m) * g.H * g.W;
+    const T *Wm = c.W + (long long)m * g.Kg;
     double acc = 0.0;
     int k = 0;
-    for (int ch = 0; ch < g.C; ++ch)
+    for (int ch = 0; ch < g.Cg; ++ch)
         for (int r = 0; r < g.R; ++r)
             for (int s = 0; s < g.S; ++s, ++k) {
                 const int ih = g.U * x + r - g.P, iw = g.U * y + s - g.P;
@@ -237,8 +238,13 @@ template <typename T> __device__ void row_arrays(const Ctx<T> &c, int p, int x, 
         const int kend = g.K - k0 < KC ? g.K - k0 : KC;
         for (int m = threadIdx.x; m < g.M; m += kThreads) {
             double a1 = c.co1m[m], a3 = c.d3[m];
-            const T *wr = c.W + (long long)m * g.K + k0;
-            for (int kk = 0; kk < kend; ++kk) {
+            // filter m's taps in the dense k = (c, r, s) order are the contiguous run of its channel
+            // group (the whole K when ungrouped); W holds them from m * Kg
+            const int kg0 = group_first_channel(g, m) * g.R * g.S;
+            const int lo = kg0 - k0 > 0 ? kg0 - k0 : 0;
+            const int hi = kg0 + g.Kg - k0 < kend ? kg0 + g.Kg - k0 : kend;
+            const T *wr = c.W + (long long)m * g.Kg + (k0 - kg0);
+            for (int kk = lo; kk < hi; ++kk) {
                 const double w = ldo(wr, kk);
                 a1 = fma(sh.win1[kk], w, a1);
                 a3 = fma(sh.win2[kk], w, a3);
@@ -431,9 +437,10 @@ __device__ bool scheme_coc(const Ctx<T> &c, Sh &sh, int p, int x, int y, const d
     double v;
     if (c.recompute) {
         double a[1] = {0.0};
-        const T *Dn = c.D + (long long)i * c.g.CHW;
-        const T *Wm = c.W + (long long)j * c.g.K;
-        for (int k = threadIdx.x; k < c.g.K; k += kThreads) {
+        // over filter j's channel group on a grouped layer (Sec. 5.2)
+        const T *Dn = c.D + (long long)i * c.g.CHW + (long long)group_first_channel(c.g, j) * c.g.H * c.g.W;
+        const T *Wm = c.W + (long long)j * c.g.Kg;
+        for (int k = threadIdx.x; k < c.g.Kg; k += kThreads) {
             const int RS = c.g.R * c.g.S;
             const int ch = k / RS, rem = k - ch * RS, r = rem / c.g.S, s = rem - r * c.g.S;
             const int ih = c.g.U * x + r - c.g.P, iw = c.g.U * y + s - c.g.P;
@@ -559,9 +566,13 @@ template <typename T> __device__ void fresh_coc(const Ctx<T> &c, int x, int y, S
             a1 += dv;
             a2 = fma((double)(n + c.wb), dv, a2);
         }
+        // Cw1, Cw2 at k: the filters whose channel group holds channel ch (all of them when
+        // ungrouped; Sec. 5.2), each read at its own offset in W [M][Cg][R][S]
+        const int grp = ch / g.Cg;
+        const long long kl = (long long)k - (long long)grp * g.Cg * RS;
 #pragma unroll 8
-        for (int m = 0; m < g.M; ++m) {
-            const double wv = ldo(c.W, (long long)m * g.K + k);
+        for (int m = grp * g.Mg; m < (grp + 1) * g.Mg; ++m) {
+            const double wv = ldo(c.W, (long long)m * g.Kg + kl);
             b1 += wv;
             b2 = fma((double)(m + c.wb), wv, b2);
         }

@@ -21,7 +21,12 @@ struct Geom {
     long long CHW;        // elements of one feature-map block D_n
     long long P_total;    // N*E*F: GEMM columns of the implicit-GEMM convolution
     int dtype, wbase;
+    // G groups (Sec. 5.2): W is [M][Cg][R][S] with Cg = C/G, Kg = Cg*R*S per filter; filter m
+    // meets channels [group_first_channel(m), + Cg).  K = C*R*S is the dense reduction of the
+    // block-diagonal expansion of W that the convolution runs on.  G = 1: Cg = C, Kg = K.
+    int G, Cg, Mg, Kg;
 };
+__host__ __device__ inline int group_first_channel(const Geom &g, int m) { return (m / g.Mg) * g.Cg; }
 
 // Tiling of the Co5..Co7 products computed by extra workgroups of the
 // convolution launch (channels-last layers): output tiles of tx columns (of F)
@@ -57,7 +62,7 @@ struct Plan {
     bool co_in_conv;                  // Co5..Co7 partials computed by workgroups of the convolution launch
     CocTile co;                       // their tiling (co_in_conv)
     size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, off_zero,
-        off_wchk, bytes;
+        off_wchk, off_wfull, bytes;
     size_t corr_stride;               // doubles of scratch per correction workgroup
 };
 
@@ -124,7 +129,7 @@ __device__ inline void reset_report(ftcnn_report *rep, int cap) {
 
 __host__ __device__ inline double tol_scale(const Geom &g, double kappa) {
     const double u_out = g.dtype == FTCNN_BF16 ? kUOutBf16 : 0.0;
-    return kappa * (kUAcc * sqrt((double)g.K) + u_out);
+    return kappa * (kUAcc * sqrt((double)g.Kg) + u_out);   // Kg: the dot length of one output
 }
 
 __device__ inline bool is_bad(double d, double q, double scale) {
@@ -147,6 +152,10 @@ hipError_t launch_encode(const Plan &pl, int which, const void *X, double *c1, d
 // bias: NULL, or fp32 [M] added to every O[n][m] before rounding (Sec. 5.1).
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st,
                        const float *bias = nullptr);
+// Grouped layers (G > 1, Sec. 5.2): the block-diagonal expansion of W ([M][Cg][R][S]) into the
+// dense [M][C][R][S] at pl.off_wfull, zeros outside each filter's channel group; returns W itself
+// when G = 1.  Its Cw1, Cw2 are the grouped checksums of Sec. 5.2.
+const void *dense_weights(const Plan &pl, const void *W, void *ws, hipStream_t st, hipError_t *err);
 // Re-encode Cw1, Cw2 of W into the workspace (pl.off_wchk) and count the columns whose Cw1
 // differs bitwise from cw1 into *mismatches (Sec. 4.1.2).
 hipError_t launch_check_weights(const Plan &pl, const void *W, const double *cw1, int32_t *mismatches, void *ws,

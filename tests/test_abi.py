@@ -63,7 +63,8 @@ def test_non_square():
 
 @pytest.mark.parametrize("kw,code", [
     (dict(n=0), -2), (dict(stride=0), -2), (dict(pad=-1), -2), (dict(r=20), -2),
-    (dict(groups=2), -6), (dict(dtype_raw=7), -3), (dict(wbase=2), -1),
+    (dict(groups=2), -2), (dict(groups=0), -2), (dict(ch=4, m=6, groups=4), -2),
+    (dict(dtype_raw=7), -3), (dict(wbase=2), -1),
 ])
 def test_bad_descriptor(kw, code):
     args = dict(n=2, ch=3, h=8, w=8, m=4, r=3, s=3, stride=1, pad=0, groups=1, dtype=ft.F32, wbase=0)
@@ -76,6 +77,13 @@ def test_bad_descriptor(kw, code):
     assert _lib.load().ftcnn_out_shape(C.byref(d), C.byref(E), C.byref(F)) == code
     assert ft.workspace_bytes(d) == 0
     assert ft.last_error()
+
+
+def test_grouped_descriptor_accepted():
+    d = ft.make_desc(2, 4, 8, 8, 6, 3, 3, groups=2)
+    assert ft.out_shape(d) == (6, 6)
+    dense = ft.workspace_bytes(ft.make_desc(2, 4, 8, 8, 6, 3, 3))
+    assert ft.workspace_bytes(d) > dense   # room for the block-diagonal expansion of W
 
 
 def test_null_pointers_rejected_without_launch():
