@@ -64,6 +64,9 @@ def parse():
                          "recomputation) on each distinct layer, and the layerwise RC/ClC choice (one JSON "
                          "line per layer)")
     ap.add_argument("--scheme-reps", type=int, default=10)
+    ap.add_argument("--groups", action="store_true",
+                    help="AlexNet with Caffe's two groups on conv2, conv4 and conv5 (Sec. 5.2); flops counted "
+                         "for the grouped layers")
     ap.add_argument("--bias", action="store_true",
                     help="give every layer a seeded bias (Sec. 5.1): the output carries it and every check "
                          "applies its shares (the workloads themselves have none)")
@@ -71,22 +74,23 @@ def parse():
 
 
 class LayerRun:
-    def __init__(self, cfg, li, ft, torch, bias=False):
+    def __init__(self, cfg, li, ft, torch, bias=False, groups=1):
         import workloads as wl
         self.spec = spec = cfg.layers[li]
         self.name = spec.name
         self.lay = ft.Layer(spec.n, spec.ch, spec.h, spec.w, spec.m, spec.r, spec.s, spec.stride,
-                            spec.pad, spec.dtype)
+                            spec.pad, spec.dtype, groups=groups)
         tdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32   # bf16 draws are exact in bf16
         self.D = torch.from_numpy(wl.gen_d(cfg, li)).to(tdt).cuda()
-        self.W = torch.from_numpy(wl.gen_w(cfg, li)).to(tdt).cuda()
+        # a grouped layer's filters see ch / groups channels (He-normal over that fan-in)
+        self.W = torch.from_numpy(wl.gen_w(cfg, li, spec.with_(ch=spec.ch // groups))).to(tdt).cuda()
         self.O = self.lay.empty_output()
         self.lay.encode_weights(self.W)
         if bias:
             b = np.random.default_rng([12203, cfg.cid, li, 5]).uniform(-0.1, 0.1, size=spec.m)
             self.lay.set_bias(torch.from_numpy(b.astype(np.float32)).cuda())
         E, F = self.lay.E, self.lay.F
-        self.flops = 2.0 * spec.n * spec.m * E * F * spec.ch * spec.r * spec.s
+        self.flops = 2.0 * spec.n * spec.m * E * F * (spec.ch // groups) * spec.r * spec.s
         d = wl.fault_draws(cfg.cid, li, 1)[0]
         self.fault = {"n": int(d[0] * spec.n), "m": int(d[1] * spec.m), "x": int(d[2] * E),
                       "y": int(d[3] * F), "kind": "add", "value": FAULT_VALUE}
@@ -155,7 +159,12 @@ def main():
     torch.cuda.set_device(0)
     cfg = {"alexnet": wl.config(1), "vgg19": wl.config(2), "vgg19_bf16": wl.vgg19_bf16(),
            "resnet18": wl.config(3), "darknet19": wl.config(4)}[args.workload]
-    runs = [LayerRun(cfg, li, ft, torch, args.bias) for li in range(len(cfg.layers))]
+    if args.groups and args.workload != "alexnet":
+        print("bench.py: --groups applies to the AlexNet workload (Caffe's two groups)", file=sys.stderr)
+        sys.exit(2)
+    grouped = ("conv2", "conv4", "conv5") if args.groups else ()
+    runs = [LayerRun(cfg, li, ft, torch, args.bias, 2 if cfg.layers[li].name in grouped else 1)
+            for li in range(len(cfg.layers))]
     if args.schemes:
         scheme_table(args, cfg, runs, ft, torch)
         return
@@ -326,7 +335,8 @@ def main():
                                f"-b{cfg.layers[0].n}",
                    "batch": cfg.layers[0].n, "layers": nl,
                    "faults_per_step": 1, "gflop_per_step": round(total_flops / 1e9, 3),
-                   **({"bias": True} if args.bias else {})},
+                   **({"bias": True} if args.bias else {}),
+                   **({"groups": {"conv2": 2, "conv4": 2, "conv5": 2}} if args.groups else {})},
         "error_free_tflops": round(total_flops / t_clean / 1e12, 3),
         "unprotected_tflops": round(total_flops / t_unprot / 1e12, 3),
         "overhead_error_free_pct": round((t_clean / t_unprot - 1) * 100, 2),
