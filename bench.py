@@ -67,6 +67,9 @@ def parse():
     ap.add_argument("--groups", action="store_true",
                     help="AlexNet with Caffe's two groups on conv2, conv4 and conv5 (Sec. 5.2); flops counted "
                          "for the grouped layers")
+    ap.add_argument("--chain", action="store_true",
+                    help="the workload's layers chained into one network (ReLU, and max pooling where "
+                         "the size drops, between layers): whole-network protected inference")
     ap.add_argument("--bias", action="store_true",
                     help="give every layer a seeded bias (Sec. 5.1): the output carries it and every check "
                          "applies its shares (the workloads themselves have none)")
@@ -168,6 +171,8 @@ def main():
     if args.schemes:
         scheme_table(args, cfg, runs, ft, torch)
         return
+    if args.chain:
+        return chain_bench(args, cfg, runs, ft, torch)
     dtype = cfg.layers[0].dtype
     peak = MFMA_PEAK[dtype]
     nl = len(runs)
@@ -353,6 +358,110 @@ def main():
     }
     print(json.dumps(out))
     return 0 if ok_fault and clean_ok else 1
+
+
+def chain_bench(args, cfg, runs, ft, torch):
+    """Whole-network protected inference: every layer protected (conv_fwd_sums with the encode,
+    verify_correct_sums with Co5..Co7) and ftcnn_relu_pool between layers, steps enqueued back to
+    back as in the single-layer measurement; the host's recomputation check (every layer's report
+    of a step) is timed on its own.  The unprotected network runs the same convolution kernels and
+    the same operations between layers."""
+    from paper_2003_12203_amd import network
+    if any(r.lay.groups > 1 for r in runs) or args.bias:
+        print("bench.py: --chain runs the dense, bias-free layers", file=sys.stderr)
+        sys.exit(2)
+    specs = [(l.n, l.ch, l.h, l.w, l.m, l.r, l.s, l.stride, l.pad) for l in cfg.layers]
+    dtype = cfg.layers[0].dtype
+    net = network.Chain(specs, dtype)
+    net.set_weights([r.W for r in runs])
+    D0 = runs[0].D
+    nl = len(runs)
+    total_flops = sum(r.flops for r in runs)
+    # the inputs of layers 1.. are the chain's own; free the per-layer bench tensors
+    for r in runs[1:]:
+        r.D = None
+    faults = [[[r.fault] if li == i % nl else [] for li, r in enumerate(runs)] for i in range(nl)]
+
+    def prot(i, inject=True):
+        net.launch(D0, faults[i % nl] if inject else None)
+
+    def plain(i):
+        net.launch_plain(D0)
+
+    def timed(fn, steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            fn(i)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps
+
+    for i in range(args.warmup):
+        prot(i)
+        plain(i)
+    # the fault-free output, for the check of the faulted steps
+    prot(0, False)
+    net.finish(D0)
+    clean_out = net.outputs[-1].float().clone()
+    t_prot = timed(prot, args.steps)
+    last = (args.steps - 1) % nl
+    reps = net.finish(D0)
+    f = runs[last].fault
+    ok_fault = all((rep.fixes == [(f["n"], f["m"], f["x"], f["y"], ft.SCHEME_COC)] and
+                    rep.status == ft.STATUS_CORRECTED) if li == last else not rep.detected
+                   for li, rep in enumerate(reps))
+    out = net.outputs[-1].float()
+    rel = float(((out - clean_out).abs().max() / clean_out.abs().max().clamp_min(1e-30)).item())
+    t_clean = timed(lambda i: prot(i, False), args.steps)
+    t_plain = timed(plain, args.steps)
+    # the host's recomputation check of one step (one synchronization, the report headers of
+    # every layer in one copy), after the GPU has finished
+    chk = []
+    for _ in range(5):
+        prot(0, False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        net.finish(D0)
+        chk.append(time.perf_counter() - t0)
+
+    # the operations between layers alone (events around them, in the unprotected pass)
+    reps_n = max(3, min(args.steps, 10))
+    link_ms = []
+    for _ in range(reps_n):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nl - 1)]
+        for l, lay in enumerate(net.layers):
+            O = net.outputs[l]
+            lay.conv_ws(D0 if l == 0 else net.inputs[l], net.W[l], O)
+            if l + 1 < nl:
+                evs[l][0].record()
+                ft.relu_pool(O, *net.links[l], Y=net.inputs[l + 1])
+                evs[l][1].record()
+        torch.cuda.synchronize()
+        link_ms.append(sum(a.elapsed_time(b) for a, b in evs))
+    res = {
+        "metric": "chained protected network, conv TFLOP/s + ABFT overhead % vs the unprotected network",
+        "value": round(total_flops / t_prot / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(t_prot * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name.split('_')[0]}-{nl}conv-chained-{'fp32' if dtype == 'f32' else 'bf16'}"
+                               f"-b{cfg.layers[0].n}",
+                   "batch": cfg.layers[0].n, "layers": nl, "links": [f"{k}x{k}/{s}" for k, s in net.links],
+                   "faults_per_step": 1, "gflop_per_step": round(total_flops / 1e9, 3)},
+        "error_free_tflops": round(total_flops / t_clean / 1e12, 3),
+        "unprotected_tflops": round(total_flops / t_plain / 1e12, 3),
+        "overhead_error_free_pct": round((t_clean / t_plain - 1) * 100, 2),
+        "overhead_erroneous_pct": round((t_prot / t_plain - 1) * 100, 2),
+        "links_ms": round(float(np.median(link_ms)), 4),
+        "host_check_ms": round(float(np.median(chk)) * 1e3, 4),
+        "timing": "steps enqueued back to back; every layer's report of the last step read after the timed "
+                  "region (host_check_ms: that read for one step)",
+        "fault_corrected": bool(ok_fault),
+        "output_rel_diff_vs_fault_free": rel,
+    }
+    print(json.dumps(res))
+    return 0 if ok_fault else 1
 
 
 def measured_traffic():

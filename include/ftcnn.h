@@ -303,6 +303,17 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
  * the caller (with timing enabled) on the device of that stream. */
 int ftcnn_set_kernel_events(hipEvent_t before, hipEvent_t after);
 
+/* Between two protected layers of a network (AlexNet, VGG-19 and Darknet-19 in
+ * Sec. 6): Y = k x k / s max pooling (no padding) of relu(X), relu(v) = v > 0 ? v : +0
+ * (NaN and both zeros give +0).  X [n][c][h][w] and Y [n][c][(h-k)/s+1][(w-k)/s+1]
+ * are device tensors of the dtype (FTCNN_F32 or FTCNN_BF16); every output is an input
+ * value or +0, so the result is exact.  (k, s) is (1, 1) (ReLU only; X == Y allowed),
+ * (2, 2) or (3, 2) (X and Y must not overlap), else FTCNN_E_UNSUPPORTED.  The next
+ * layer then encodes its Cd1, Cd2 from Y, the corrected output of this layer after
+ * these operations. */
+int ftcnn_relu_pool(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s,
+                    const void *X, void *Y, hipStream_t stream);
+
 /* TEST ONLY: corrupt stored outputs, reproducing the paper's source-level
  * fault injection (Sec. 6.1).  faults is a HOST array of at most 64 entries
  * (ftcnn_fault above), applied in order.  Positions must be in range. */

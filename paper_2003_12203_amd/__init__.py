@@ -123,6 +123,27 @@ def conv_fwd_bias(desc, D, W, bias, O, workspace=None, stream=None) -> None:
                                      _stream(stream)), "ftcnn_conv_fwd_bias")
 
 
+def relu_pool(X: torch.Tensor, k: int = 1, s: int = 1, Y: Optional[torch.Tensor] = None,
+              stream=None) -> torch.Tensor:
+    """ftcnn_relu_pool: k x k / s max pooling of relu(X) (k = s = 1: ReLU only), the operations
+    between two layers of a network.  X is [n][c][h][w] (float32, or bfloat16); Y is allocated
+    when not given."""
+    if X.dim() != 4 or not X.is_contiguous():
+        raise FtcnnError("relu_pool: X must be a contiguous [n][c][h][w] tensor")
+    dt = {torch.float32: "f32", torch.bfloat16: "bf16"}.get(X.dtype)
+    if dt is None:
+        raise FtcnnError(f"relu_pool: dtype {X.dtype}")
+    n, c, h, w = X.shape
+    shape = (n, c, (h - k) // s + 1, (w - k) // s + 1)
+    if Y is None:
+        Y = torch.empty(shape, dtype=X.dtype, device=X.device)
+    elif tuple(Y.shape) != shape or Y.dtype != X.dtype or not Y.is_contiguous():
+        raise FtcnnError(f"relu_pool: Y must be a contiguous {shape} tensor of {X.dtype}")
+    _check(lib().ftcnn_relu_pool(DTYPES[dt][0], n, c, h, w, k, s, _ptr(X), _ptr(Y), _stream(stream)),
+           "ftcnn_relu_pool")
+    return Y
+
+
 def conv_fwd_ws(desc, D, W, O, workspace, stream=None) -> None:
     _check(lib().ftcnn_conv_fwd_ws(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), _ptr(workspace), _stream(stream)),
            "ftcnn_conv_fwd_ws")

@@ -56,7 +56,8 @@ class Fault(C.Structure):
 EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ftcnn_last_error",
            "ftcnn_encode", "ftcnn_conv_fwd", "ftcnn_checksum_conv", "ftcnn_verify", "ftcnn_correct",
            "ftcnn_verify_correct", "ftcnn_conv_fwd_ws", "ftcnn_conv_fwd_sums", "ftcnn_verify_correct_sums", "ftcnn_protected_conv",
-           "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias", "ftcnn_check_weights")
+           "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias", "ftcnn_check_weights",
+           "ftcnn_relu_pool")
 
 _lib = None
 
@@ -94,6 +95,8 @@ def load(path: str = LIB_PATH):
     L.ftcnn_verify_correct.restype = C.c_int
     L.ftcnn_check_weights.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp]
     L.ftcnn_check_weights.restype = C.c_int
+    L.ftcnn_relu_pool.argtypes = [C.c_int32] * 7 + [_dp, _dp, _dp]
+    L.ftcnn_relu_pool.restype = C.c_int
     L.ftcnn_conv_fwd_bias.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp, _dp]
     L.ftcnn_conv_fwd_bias.restype = C.c_int
     L.ftcnn_conv_fwd_ws.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp]

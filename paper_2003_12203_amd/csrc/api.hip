@@ -501,4 +501,25 @@ int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults
     return FTCNN_OK;
 }
 
+int ftcnn_relu_pool(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s, const void *X,
+                    void *Y, hipStream_t stream) {
+    if (dtype != FTCNN_F32 && dtype != FTCNN_BF16) return fail(FTCNN_E_DTYPE, "relu_pool: dtype %d", dtype);
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return fail(FTCNN_E_SHAPE, "relu_pool: non-positive dimension");
+    if (!((k == 1 && s == 1) || (k == 2 && s == 2) || (k == 3 && s == 2)))
+        return fail(FTCNN_E_UNSUPPORTED, "relu_pool: window %d stride %d (1/1, 2/2 and 3/2 are built)", k, s);
+    if (h < k || w < k) return fail(FTCNN_E_SHAPE, "relu_pool: %dx%d map smaller than the %dx%d window", h, w, k, k);
+    if ((long long)n * c * h * w > (1LL << 40)) return fail(FTCNN_E_SHAPE, "relu_pool: tensor too large");
+    if (!X || !Y) return fail(FTCNN_E_ARG, "relu_pool: null pointer");
+    if (k > 1) {
+        // pooling reads windows of X while writing Y: the two must not overlap
+        const long long es = dtype == FTCNN_F32 ? 4 : 2;
+        const char *x0 = static_cast<const char *>(X), *y0 = static_cast<const char *>(Y);
+        const long long xb = (long long)n * c * h * w * es;
+        const long long yb = (long long)n * c * ((h - k) / s + 1) * ((w - k) / s + 1) * es;
+        if (x0 < y0 + yb && y0 < x0 + xb) return fail(FTCNN_E_ARG, "relu_pool: X and Y overlap");
+    }
+    FT_HIP(launch_relu_pool((ftcnn_dtype)dtype, X, Y, n, c, h, w, k, s, stream), "relu_pool");
+    return FTCNN_OK;
+}
+
 }  // extern "C"

@@ -156,6 +156,9 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
 // dense [M][C][R][S] at pl.off_wfull, zeros outside each filter's channel group; returns W itself
 // when G = 1.  Its Cw1, Cw2 are the grouped checksums of Sec. 5.2.
 const void *dense_weights(const Plan &pl, const void *W, void *ws, hipStream_t st, hipError_t *err);
+// ReLU then k x k / s max pooling between two layers of a network (k = s = 1: ReLU only)
+hipError_t launch_relu_pool(ftcnn_dtype dt, const void *X, void *Y, int n, int c, int h, int w, int k, int s,
+                            hipStream_t st);
 // Re-encode Cw1, Cw2 of W into the workspace (pl.off_wchk) and count the columns whose Cw1
 // differs bitwise from cw1 into *mismatches (Sec. 4.1.2).
 hipError_t launch_check_weights(const Plan &pl, const void *W, const double *cw1, int32_t *mismatches, void *ws,

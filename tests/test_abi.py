@@ -108,3 +108,25 @@ def test_null_pointers_rejected_without_launch():
     ws_mis = C.c_void_p(256 + 8)
     assert L.ftcnn_verify(C.byref(d), C.c_void_p(256), C.byref(ck), C.byref(pol), C.c_void_p(256), 4,
                           ws_mis, None) == -1  # ck arrays missing are reported first
+
+
+def test_relu_pool_rejects_bad_arguments_without_launch():
+    L = _lib.load()
+    X, Y = C.c_void_p(1 << 20), C.c_void_p(1 << 24)
+    assert L.ftcnn_relu_pool(ft.F32, 2, 3, 8, 8, 4, 4, X, Y, None) == -6      # window not built
+    assert L.ftcnn_relu_pool(ft.F32, 2, 3, 8, 8, 3, 1, X, Y, None) == -6
+    assert L.ftcnn_relu_pool(7, 2, 3, 8, 8, 2, 2, X, Y, None) == -3           # dtype
+    assert L.ftcnn_relu_pool(ft.BF16, 2, 0, 8, 8, 2, 2, X, Y, None) == -2     # empty
+    assert L.ftcnn_relu_pool(ft.BF16, 2, 3, 2, 8, 3, 2, X, Y, None) == -2     # map below the window
+    assert L.ftcnn_relu_pool(ft.F32, 2, 3, 8, 8, 2, 2, None, Y, None) == -1
+    # pooling in place (or into an overlapping range) would read windows already overwritten
+    assert L.ftcnn_relu_pool(ft.F32, 2, 3, 8, 8, 2, 2, X, X, None) == -1
+    assert L.ftcnn_relu_pool(ft.F32, 2, 3, 8, 8, 2, 2, X, C.c_void_p((1 << 20) + 4 * 2 * 3 * 64 - 4), None) == -1
+
+
+def test_chain_shapes_checked_on_host():
+    from paper_2003_12203_amd import network
+    assert network.pooling(55, 27) == (3, 2) and network.pooling(224, 112) == (2, 2)
+    assert network.pooling(13, 13) == (1, 1)
+    with pytest.raises(ft.FtcnnError):
+        network.pooling(8, 3)

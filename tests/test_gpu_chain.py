@@ -1,0 +1,139 @@
+"""Chained protected inference on the GPU (ftcnn_relu_pool between protected layers) against the
+oracle's chain.
+
+* ftcnn_relu_pool equals the oracle's ReLU + max pooling bit for bit (fp32 and bf16; 1x1, 2x2/2,
+  3x3/2; odd sizes; negative values, signed zeros, NaN; ReLU in place);
+* a three-layer chain on integer data (fp32, every value exact): with a fault planted in every
+  layer each layer's fixes are the oracle's, each layer's input is the oracle's, and the output is
+  the fault-free chain's bit for bit; the AlexNet-style 3x3/2 pooling chain as well;
+* a bf16 chain (channels-last layers) within the bf16 tolerance, fixes equal to the oracle's;
+* a layer beyond every scheme is recomputed and the layers after it run again on its clean output.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2003_12203_amd as ft
+from gpu_util import TOL, assert_close_scaled, dev, host
+from oracle import chain as och
+from oracle import workflow as wf
+from paper_2003_12203_amd import network, schemes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("k,s,h,w", [(1, 1, 7, 9), (1, 1, 16, 16), (2, 2, 8, 8), (2, 2, 11, 13), (3, 2, 27, 27),
+                                     (3, 2, 10, 7)])
+def test_relu_pool_matches_oracle(dt, k, s, h, w):
+    g = np.random.default_rng([12203, 95, k, h, w])
+    x = g.normal(size=(3, 5, h, w)).astype(np.float32)
+    x.flat[::17] = -0.0
+    x.flat[5::31] = np.nan
+    X = dev(x, dt)
+    print(f"[relu_pool] {dt} k={k} s={s} {h}x{w}", flush=True)
+    Y = ft.relu_pool(X, k, s)
+    ref = och.link(host(X), k, s)
+    got = host(Y)
+    np.testing.assert_array_equal(got, ref)
+    assert not np.signbit(got).any()
+    if k == 1:
+        ft.relu_pool(X, 1, 1, Y=X)   # in place
+        iv = torch.int16 if dt == "bf16" else torch.int32
+        assert torch.equal(X.view(iv), Y.view(iv))
+
+
+def _specs(n, chs, hs, rs, pads):
+    return [(n, chs[l], hs[l], hs[l], chs[l + 1], rs[l], rs[l], 1, pads[l]) for l in range(len(rs))]
+
+
+def _weights(chs, rs, seed, integer, dt):
+    g = np.random.default_rng([12203, 96, seed])
+    Ws = []
+    for l, r in enumerate(rs):
+        shape = (chs[l + 1], chs[l], r, r)
+        if integer:   # sparse small integers: every partial sum of three layers stays below 2^24
+            W = g.integers(-1, 2, size=shape) * (g.random(shape) < 0.2)
+        else:
+            W = g.normal(size=shape) * np.sqrt(2.0 / (chs[l] * r * r))
+        Ws.append(host(dev(W, dt)))   # the values the device holds
+    return Ws
+
+
+def _faults(ch_out, n, es):
+    # one large fault per layer at a different block and position (CoC-locatable)
+    return [[{"n": (2 * l + 1) % n, "m": (5 * l + 3) % ch_out[l], "x": es[l] // 2, "y": (es[l] - 1) // 3,
+              "kind": "add", "value": float(2 ** 20)}] for l in range(len(ch_out))]
+
+
+def _oracle_faults(fl):
+    return [[wf.Fault(f["n"], f["m"], f["x"], f["y"], "add", value=f["value"]) for f in layer] for layer in fl]
+
+
+CHAINS = [
+    # n, channels, input sizes, kernel sizes, pads, dtype
+    (4, (3, 32, 64, 32), (16, 16, 8), (3, 3, 3), (1, 1, 1), "f32"),       # VGG-style 2x2/2 between 2 and 3
+    (3, (3, 16, 32, 24), (15, 7, 7), (3, 3, 1), (1, 1, 0), "f32"),        # AlexNet-style 3x3/2, then a 1x1
+    (4, (64, 64, 128, 64), (12, 12, 6), (3, 3, 3), (1, 1, 1), "f32"),     # channels-last copies
+]
+
+
+@pytest.mark.parametrize("case", CHAINS, ids=lambda c: f"{c[0]}-{'-'.join(map(str, c[1]))}-{c[5]}")
+def test_chain_integer_matches_oracle(case):
+    n, chs, hs, rs, pads, dt = case
+    specs = _specs(n, chs, hs, rs, pads)
+    net = network.Chain(specs, dt)
+    Ws = _weights(chs, rs, sum(chs), True, dt)
+    D0 = np.random.default_rng([12203, 97, n]).integers(0, 3, size=(n, chs[0], hs[0], hs[0])).astype(np.float64)
+    net.set_weights([dev(W, dt) for W in Ws])
+    es = [lay.E for lay in net.layers]
+    fl = _faults(chs[1:], n, es)
+    print(f"[chain] {case}", flush=True)
+    out, reps = net.run(dev(D0, dt), fl)
+    ref = och.protect_chain(D0, Ws, [1] * len(rs), list(pads), net.links, dt, faults=_oracle_faults(fl))
+    clean = och.protect_chain(D0, Ws, [1] * len(rs), list(pads), net.links, dt)
+    assert net.links == och.links_for([(hs[l], rs[l], 1, pads[l], chs[l + 1]) for l in range(len(rs))])
+    for l, (rep, r) in enumerate(zip(reps, ref.layers)):
+        f = fl[l][0]
+        assert rep.fixes == r.report.fixes == [(f["n"], f["m"], f["x"], f["y"], ft.SCHEME_COC)], l
+        assert rep.status == ft.STATUS_CORRECTED
+        if l > 0:
+            np.testing.assert_array_equal(host(net.inputs[l]), ref.inputs[l])
+        np.testing.assert_array_equal(net.layers[l].buf["cd1"].cpu().numpy(), ref.layers[l].ck.cd1.ravel())
+    np.testing.assert_array_equal(host(out), clean.output)
+
+
+def test_chain_bf16_matches_oracle():
+    n, chs, hs, rs, pads, dt = 4, (64, 64, 128, 64), (16, 16, 8), (3, 3, 3), (1, 1, 1), "bf16"
+    net = network.Chain(_specs(n, chs, hs, rs, pads), dt)
+    Ws = _weights(chs, rs, 7, False, dt)
+    D0 = host(dev(np.random.default_rng([12203, 98]).uniform(0, 1, size=(n, chs[0], hs[0], hs[0])), dt))
+    net.set_weights([dev(W, dt) for W in Ws])
+    fl = _faults(chs[1:], n, [lay.E for lay in net.layers])
+    for f in fl:
+        f[0]["value"] = float(2 ** 12)   # large against these outputs, exact in bf16
+    out, reps = net.run(dev(D0, dt), fl)
+    ref = och.protect_chain(D0, Ws, [1] * 3, list(pads), net.links, dt, faults=_oracle_faults(fl))
+    for l, (rep, r) in enumerate(zip(reps, ref.layers)):
+        assert rep.fixes == r.report.fixes and len(rep.fixes) == 1, l
+        assert rep.status == ft.STATUS_CORRECTED
+    assert_close_scaled(host(out), ref.output, TOL[dt], "chain output")
+
+
+def test_chain_recomputes_and_runs_on():
+    n, chs, hs, rs, pads, dt = 6, (3, 16, 8), (9, 9), (3, 3), (1, 1), "f32"
+    net = network.Chain(_specs(n, chs, hs, rs, pads), dt, ft.make_policy(rc_on=False, clc_on=False))
+    Ws = _weights(chs, rs, 11, True, dt)
+    D0 = np.random.default_rng([12203, 99]).integers(0, 3, size=(n, chs[0], 9, 9)).astype(np.float64)
+    net.set_weights([dev(W, dt) for W in Ws])
+    lay = net.layers[0]
+    pat = schemes.pattern("square", n, chs[1], lay.E, lay.F)
+    out, reps = net.run(dev(D0, dt), [pat, []])
+    assert reps[0].status == ft.STATUS_RECOMPUTED and not reps[1].detected
+    clean = och.protect_chain(D0, Ws, [1, 1], list(pads), net.links, dt)
+    np.testing.assert_array_equal(host(net.inputs[1]), clean.inputs[1])
+    np.testing.assert_array_equal(host(out), clean.output)
+    # and the plain network (no ABFT work) gives the same output
+    net.launch_plain(dev(D0, dt))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(net.outputs[-1]), clean.output)
