@@ -744,8 +744,8 @@ __device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double 
 //
 // TPP threads share a position, and consecutive threads take consecutive
 // positions (thread t: position t % per, lane t / per), so every load of a
-// partial slice is a coalesced run; the lanes of a position are then added by
-// a fixed tree in LDS.
+// partial slice is a coalesced run; the lanes of a position are then added in a
+// fixed order (exchanges inside each wave, then the four waves).
 template <typename T, int TPP, bool COC>
 __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int splits, const double *__restrict__ part,
                                                                   const double *__restrict__ copart, int max_groups,
@@ -755,7 +755,7 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
                                                                   size_t stride, int nslots) {
     __shared__ Sh sh;
     constexpr int NV = COC ? 7 : 4;
-    __shared__ double red[TPP > 1 ? NV : 1][TPP > 1 ? kThreads : 1];
+    __shared__ double red[TPP > 1 ? NV : 1][TPP > 1 ? 4 * (kThreads / TPP) : 1];
     const Geom &g = c.g;
     constexpr int per = kThreads / TPP;
     const int slot = threadIdx.x % per, lane = threadIdx.x / per;
@@ -764,6 +764,23 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
 #pragma unroll
     for (int i = 0; i < NV; ++i) v[i] = 0.0;
     if (p < g.EF) {
+        // the So partials first: their loads do not wait on the report word that counts the Co
+        // partials.  Four slices of loads in flight, added in slice order.
+        for (int s0 = lane; s0 < splits; s0 += 4 * TPP) {
+            double x[4][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int s = s0 + u * TPP;
+                const double *ps = part + (size_t)(s < splits ? s : 0) * 4 * g.EF + p;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) x[u][i] = ps[i * (size_t)g.EF];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (s0 + u * TPP < splits)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] += x[u][i];
+        }
         if constexpr (COC) {
             // slices written by the convolution launch that reset this report (never more than
             // the workspace holds)
@@ -792,36 +809,24 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
                 coc_taps<T, TPP>(c, lane, x, p - x * g.F, v[4], v[5], v[6]);
             }
         }
-        // four slices of loads in flight, added in slice order
-        for (int s0 = lane; s0 < splits; s0 += 4 * TPP) {
-            double x[4][4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int s = s0 + u * TPP;
-                const double *ps = part + (size_t)(s < splits ? s : 0) * 4 * g.EF + p;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) x[u][i] = ps[i * (size_t)g.EF];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (s0 + u * TPP < splits)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] += x[u][i];
-        }
     }
     if constexpr (TPP > 1) {
+        // the TPP lanes of a position are the threads t = slot (mod per): inside a wave they are
+        // folded by exchanges at distances per, 2 per, ..., 32, then the four waves' sums are
+        // added in wave order (a fixed order: the same sums on every run)
+        static_assert(kThreads == 256 && TPP >= 4, "four waves, at most 64 positions a workgroup");
 #pragma unroll
-        for (int i = 0; i < NV; ++i) red[i][threadIdx.x] = v[i];
+        for (int o = per; o < 64; o <<= 1)
 #pragma unroll
-        for (int h = TPP / 2; h > 0; h >>= 1) {
-            __syncthreads();
-            if (lane < h)
+            for (int i = 0; i < NV; ++i) v[i] += __shfl_xor(v[i], o, 64);
+        const int wv = threadIdx.x >> 6, wl = threadIdx.x & 63;
+        if (wl < per)
 #pragma unroll
-                for (int i = 0; i < NV; ++i) red[i][threadIdx.x] += red[i][threadIdx.x + h * per];
-        }
+            for (int i = 0; i < NV; ++i) red[i][wv * per + wl] = v[i];
         __syncthreads();
 #pragma unroll
-        for (int i = 0; i < NV; ++i) v[i] = red[i][slot];
+        for (int i = 0; i < NV; ++i)
+            v[i] = ((red[i][slot] + red[i][per + slot]) + red[i][2 * per + slot]) + red[i][3 * per + slot];
     }
     double a = v[0], b = v[1], cc = v[2], d = v[3];
     double c5 = 0.0, c6 = 0.0, c7 = 0.0;
