@@ -22,7 +22,9 @@
  *   O [n][m][E][F] with E = floor((h + 2*pad - r)/stride) + 1 and
  *   F = floor((w + 2*pad - s)/stride) + 1.  D, W and O share the dtype of the
  *   descriptor (fp32, or bf16 as raw 16-bit patterns); accumulation is fp32 in
- *   the convolution and fp64 everywhere on the checksum side.
+ *   the convolution and fp64 everywhere on the checksum side, except that a
+ *   bf16 layer's convolution epilogue adds each run of 16 filters of a pixel in
+ *   fp32 (every term exact; at most 15 roundings of 2^-24 a run) before fp64.
  * - Checksum arrays are float64: Cd1, Cd2 [ch][h][w]; Cw1, Cw2 [ch][r][s];
  *   Co5, Co6, Co7, So5, So6, So7, Q5 [E][F]; Co1, Co3 [m][E][F];
  *   Co2, Co4 [n][E][F].

@@ -831,26 +831,65 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             s1[j] = s6[j] = sq[j] = 0.0;
         }
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int i = 0; i < FM; ++i) {
+            if constexpr (sizeof(T) == 2) {
+                // bf16 outputs: the 16 rows of a block are first summed in fp32, then added in
+                // fp64.  Every term is exact in fp32 (8-bit values, weights m + wbase below 2^16),
+                // so the only roundings are the 15 additions of a run: at most 15 * 2^-24 of the
+                // run's sum of magnitudes, far inside the bf16 tolerance (whose output unit is
+                // 2^-8), and none at all while the partial sums stay integers below 2^24.  The
+                // fp64 arithmetic per element would otherwise cost as much as a third of the
+                // matrix-core time on short-K layers.
+                float f1[FP], f6[FP], fq[FP];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int mo = i * 32 + 8 * (e >> 2) + (e & 3);   // row offset from mrow
-                const int m = mrow + mo;
-                const bool mok = m < g.M;
-                const double wm = (double)m + wb;
-                const float bm = hb ? bias_s[m - m0] : 0.0f;
+                for (int j = 0; j < FP; ++j) f1[j] = f6[j] = fq[j] = 0.0f;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int mo = i * 32 + 8 * (e >> 2) + (e & 3);   // row offset from mrow
+                    const int m = mrow + mo;
+                    const bool mok = m < g.M;
+                    const float wm = (float)(m + g.wbase);
+                    const float bm = hb ? bias_s[m - m0] : 0.0f;
+#pragma unroll
+                    for (int j = 0; j < FP; ++j) {
+                        const typename Bt::B b = Bt::make(hb ? acc[i][j][e] + bm : acc[i][j][e]);
+                        if (cval[j] && mok) {
+                            const float v = Bt::value(b);
+                            f1[j] += v;
+                            f6[j] = fmaf(wm, v, f6[j]);
+                            fq[j] = fmaf(v, v, fq[j]);
+                            obase[j][mo * g.EF] = b;
+                        }
+                    }
+                }
 #pragma unroll
                 for (int j = 0; j < FP; ++j) {
-                    const typename Bt::B b = Bt::make(hb ? acc[i][j][e] + bm : acc[i][j][e]);
-                    if (cval[j] && mok) {
-                        const double v = (double)Bt::value(b);
-                        s1[j] += v;
-                        s6[j] = fma(wm, v, s6[j]);
-                        sq[j] = fma(v, v, sq[j]);
-                        obase[j][mo * g.EF] = b;
+                    s1[j] += (double)f1[j];
+                    s6[j] += (double)f6[j];
+                    sq[j] += (double)fq[j];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int mo = i * 32 + 8 * (e >> 2) + (e & 3);   // row offset from mrow
+                    const int m = mrow + mo;
+                    const bool mok = m < g.M;
+                    const double wm = (double)m + wb;
+                    const float bm = hb ? bias_s[m - m0] : 0.0f;
+#pragma unroll
+                    for (int j = 0; j < FP; ++j) {
+                        const typename Bt::B b = Bt::make(hb ? acc[i][j][e] + bm : acc[i][j][e]);
+                        if (cval[j] && mok) {
+                            const double v = (double)Bt::value(b);
+                            s1[j] += v;
+                            s6[j] = fma(wm, v, s6[j]);
+                            sq[j] = fma(v, v, sq[j]);
+                            obase[j][mo * g.EF] = b;
+                        }
                     }
                 }
             }
+        }
 #pragma unroll
         for (int j = 0; j < FP; ++j) {
             // rows 4..7 of every 8 sit in the other half-wave: both halves end with the same sums

@@ -16,7 +16,7 @@ import torch
 
 import paper_2003_12203_amd as ft
 import workloads as wl
-from gpu_util import TOL, dev, layer_for
+from gpu_util import EPI_RUN_EPS, TOL, dev, layer_for
 from oracle import core
 from oracle import workflow as wf
 
@@ -91,8 +91,13 @@ def test_full_size_layer(cfg, li):
     for name, refv in (("co5", co5), ("co6", co6), ("co7", co7)):
         lim = 1e-11 * (np.abs(refv) + big * q + 1e-300)
         assert np.all(np.abs(b[name][flat] - refv) <= lim), name
+    # bf16: the epilogue's fp32 runs of 16 filters (every term exact, 15 roundings a run)
+    mag = np.abs(blocks)
+    eps = EPI_RUN_EPS if dt == "bf16" else 0.0
+    slack = {"so5": eps * mag.sum(axis=(0, 1)), "so6": eps * (wm * mag).sum(axis=(0, 1)),
+             "so7": eps * (wn * mag).sum(axis=(0, 1))}
     for name, refv in (("so5", so5), ("so6", so6), ("so7", so7)):
-        lim = 1e-11 * (np.abs(refv) + big * q + 1e-300)
+        lim = 1e-11 * (np.abs(refv) + big * q + 1e-300) + slack[name]
         assert np.all(np.abs(b[name][flat] - refv) <= lim), name
 
     # the benchmark's fault: planted in the convolution's output, detected and repaired by CoC
