@@ -403,7 +403,23 @@ def chain_bench(args, cfg, runs, ft, torch):
     prot(0, False)
     net.finish(D0)
     clean_out = net.outputs[-1].float().clone()
-    t_prot = timed(prot, args.steps)
+    def copy_clean(i):
+        net.fuse_encode = False
+        prot(i, False)
+        net.fuse_encode = True
+
+    # the four variants timed in turns (rounds of a quarter of the steps each), so that a drift
+    # of the clock over the run falls on all of them alike
+    fns = [prot, lambda i: prot(i, False), plain, copy_clean]
+    tot = [0.0] * len(fns)
+    per = max(1, args.steps // 4)
+    for _ in range(4):
+        for k, fn in enumerate(fns):
+            tot[k] += timed(fn, per)
+    t_prot, t_clean, t_plain, t_copy = (t / 4 for t in tot)
+    # the fault of the last faulted step: run the faulted steps once more, in order
+    for i in range(args.steps):
+        prot(i)
     last = (args.steps - 1) % nl
     reps = net.finish(D0)
     f = runs[last].fault
@@ -412,8 +428,6 @@ def chain_bench(args, cfg, runs, ft, torch):
                    for li, rep in enumerate(reps))
     out = net.outputs[-1].float()
     rel = float(((out - clean_out).abs().max() / clean_out.abs().max().clamp_min(1e-30)).item())
-    t_clean = timed(lambda i: prot(i, False), args.steps)
-    t_plain = timed(plain, args.steps)
     # the host's recomputation check of one step (one synchronization, the report headers of
     # every layer in one copy), after the GPU has finished
     chk = []
@@ -454,9 +468,15 @@ def chain_bench(args, cfg, runs, ft, torch):
         "overhead_error_free_pct": round((t_clean / t_plain - 1) * 100, 2),
         "overhead_erroneous_pct": round((t_prot / t_plain - 1) * 100, 2),
         "links_ms": round(float(np.median(link_ms)), 4),
+        "encode": "the link after each layer encodes the next layer's Cd1, Cd2 (ftcnn_relu_pool_encode, "
+                  "ftcnn_conv_fwd_sums_given); the first layer encodes in its channels-last copy",
+        "copy_encode": {"error_free_tflops": round(total_flops / t_copy / 1e12, 3),
+                        "overhead_error_free_pct": round((t_copy / t_plain - 1) * 100, 2),
+                        "note": "each layer encodes its input in its own channels-last copy"},
         "host_check_ms": round(float(np.median(chk)) * 1e3, 4),
-        "timing": "steps enqueued back to back; every layer's report of the last step read after the timed "
-                  "region (host_check_ms: that read for one step)",
+        "timing": "steps enqueued back to back, the four variants (faulted, error-free, unprotected, copy-encode) "
+                  "in four rounds of turns; every layer's report of a faulted run read after the timed region "
+                  "(host_check_ms: that read for one step)",
         "fault_corrected": bool(ok_fault),
         "output_rel_diff_vs_fault_free": rel,
     }

@@ -272,6 +272,16 @@ int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *
                         const ftcnn_checksums *ck, ftcnn_report *rep, int32_t cap_fixes,
                         const ftcnn_fault *faults, int32_t nf, void *workspace, hipStream_t stream);
 
+/* ftcnn_conv_fwd_sums for a layer whose input checksums are already encoded:
+ * ck->cd1 and ck->cd2 (required) hold Cd1, Cd2 of D as inputs, for instance from
+ * ftcnn_relu_pool_encode of the layer before (Sec. 3.2), and are not written.  The
+ * channels-last copy of D then only copies, and no encode or combine workgroups run;
+ * everything else is as ftcnn_conv_fwd_sums (same O, same sums, Co5..Co7 partials when
+ * ck->cw1 and ck->cw2 are set).  Follow it with ftcnn_verify_correct_sums. */
+int ftcnn_conv_fwd_sums_given(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                              const ftcnn_checksums *ck, ftcnn_report *rep, int32_t cap_fixes,
+                              const ftcnn_fault *faults, int32_t nf, void *workspace, hipStream_t stream);
+
 /* ftcnn_verify_correct over the partial sums that ftcnn_conv_fwd_sums left in
  * the workspace (one launch; O is read only at flagged positions).  The
  * report must be the one ftcnn_conv_fwd_sums reset.  which = 0: Co5..Co7 are
@@ -315,6 +325,17 @@ int ftcnn_set_kernel_events(hipEvent_t before, hipEvent_t after);
  * these operations. */
 int ftcnn_relu_pool(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s,
                     const void *X, void *Y, hipStream_t stream);
+
+/* ftcnn_relu_pool, and with it the input checksums of the layer that reads Y
+ * (Sec. 3.2): cd1[c][i][j] = sum_n Y[n][c][i][j] and cd2[c][i][j] = sum_n (n + wbase)
+ * Y[n][c][i][j], float64 device arrays of c * ((h-k)/s+1) * ((w-k)/s+1) elements, the
+ * images added in order.  Y is the corrected output of one layer after the operations
+ * between layers, so the next layer's checksums come from the values it will read, in the
+ * pass that writes them; pass them to that layer's ftcnn_conv_fwd_sums_given.  wbase is
+ * 0 or 1 (the next layer's descriptor's). */
+int ftcnn_relu_pool_encode(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s,
+                           int32_t wbase, const void *X, void *Y, double *cd1, double *cd2,
+                           hipStream_t stream);
 
 /* TEST ONLY: corrupt stored outputs, reproducing the paper's source-level
  * fault injection (Sec. 6.1).  faults is a HOST array of at most 64 entries

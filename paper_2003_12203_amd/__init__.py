@@ -124,10 +124,11 @@ def conv_fwd_bias(desc, D, W, bias, O, workspace=None, stream=None) -> None:
 
 
 def relu_pool(X: torch.Tensor, k: int = 1, s: int = 1, Y: Optional[torch.Tensor] = None,
-              stream=None) -> torch.Tensor:
+              stream=None, cd=None, wbase: int = 0) -> torch.Tensor:
     """ftcnn_relu_pool: k x k / s max pooling of relu(X) (k = s = 1: ReLU only), the operations
     between two layers of a network.  X is [n][c][h][w] (float32, or bfloat16); Y is allocated
-    when not given."""
+    when not given.  cd = (cd1, cd2): ftcnn_relu_pool_encode, which also writes the next layer's
+    input checksums of Y there (float64 [c][h'][w'])."""
     if X.dim() != 4 or not X.is_contiguous():
         raise FtcnnError("relu_pool: X must be a contiguous [n][c][h][w] tensor")
     dt = {torch.float32: "f32", torch.bfloat16: "bf16"}.get(X.dtype)
@@ -139,8 +140,17 @@ def relu_pool(X: torch.Tensor, k: int = 1, s: int = 1, Y: Optional[torch.Tensor]
         Y = torch.empty(shape, dtype=X.dtype, device=X.device)
     elif tuple(Y.shape) != shape or Y.dtype != X.dtype or not Y.is_contiguous():
         raise FtcnnError(f"relu_pool: Y must be a contiguous {shape} tensor of {X.dtype}")
-    _check(lib().ftcnn_relu_pool(DTYPES[dt][0], n, c, h, w, k, s, _ptr(X), _ptr(Y), _stream(stream)),
-           "ftcnn_relu_pool")
+    if cd is None:
+        _check(lib().ftcnn_relu_pool(DTYPES[dt][0], n, c, h, w, k, s, _ptr(X), _ptr(Y), _stream(stream)),
+               "ftcnn_relu_pool")
+        return Y
+    cd1, cd2 = cd
+    plane = c * shape[2] * shape[3]
+    for t in (cd1, cd2):
+        if t.dtype != torch.float64 or t.numel() != plane or not t.is_contiguous():
+            raise FtcnnError(f"relu_pool: checksums must be contiguous float64 of {plane} elements")
+    _check(lib().ftcnn_relu_pool_encode(DTYPES[dt][0], n, c, h, w, k, s, wbase, _ptr(X), _ptr(Y), _ptr(cd1),
+                                        _ptr(cd2), _stream(stream)), "ftcnn_relu_pool_encode")
     return Y
 
 
@@ -149,12 +159,14 @@ def conv_fwd_ws(desc, D, W, O, workspace, stream=None) -> None:
            "ftcnn_conv_fwd_ws")
 
 
-def conv_fwd_sums(desc, D, W, O, ck, report, cap, workspace, faults: Sequence[dict] = (), stream=None) -> None:
+def conv_fwd_sums(desc, D, W, O, ck, report, cap, workspace, faults: Sequence[dict] = (), stream=None,
+                  given: bool = False) -> None:
+    """ftcnn_conv_fwd_sums; given=True: ftcnn_conv_fwd_sums_given (Cd1, Cd2 in ck are inputs)."""
     arr = _fault_array(faults)
-    _check(lib().ftcnn_conv_fwd_sums(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck) if ck else None,
-                                     _ptr(report), cap, arr if faults else None, len(faults), _ptr(workspace),
-                                     _stream(stream)),
-           "ftcnn_conv_fwd_sums")
+    fn = lib().ftcnn_conv_fwd_sums_given if given else lib().ftcnn_conv_fwd_sums
+    _check(fn(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck) if ck else None,
+              _ptr(report), cap, arr if faults else None, len(faults), _ptr(workspace), _stream(stream)),
+           "ftcnn_conv_fwd_sums_given" if given else "ftcnn_conv_fwd_sums")
 
 
 def verify_correct_sums(desc, D, W, O, ck, policy, report, workspace, which: int = 0, stream=None) -> None:
@@ -340,17 +352,19 @@ class Layer:
         else:
             conv_fwd_ws(self.desc, D, W, O, self.workspace, stream)
 
-    def conv_sums(self, D, W, O, faults=(), stream=None, encode=False):
+    def conv_sums(self, D, W, O, faults=(), stream=None, encode=False, given=False):
         """ftcnn_conv_fwd_sums; encode=True also encodes Cd1, Cd2 of D in the same pass and, on
-        channels-last layers, computes the Co5..Co7 partials from them and Cw1, Cw2."""
+        channels-last layers, computes the Co5..Co7 partials from them and Cw1, Cw2.  given=True:
+        ftcnn_conv_fwd_sums_given, with this layer's Cd1, Cd2 already encoded (by
+        relu_pool(..., cd=...) of the layer before)."""
         ck = None
-        if encode or self.bias is not None:
+        if encode or given or self.bias is not None:
             ck = _lib.Checksums()
-            if encode:
+            if encode or given:
                 ck.cd1, ck.cd2 = self.buf["cd1"].data_ptr(), self.buf["cd2"].data_ptr()
                 ck.cw1, ck.cw2 = self.buf["cw1"].data_ptr(), self.buf["cw2"].data_ptr()
             ck.bias, ck.cb = self.ck.bias, self.ck.cb   # the layer's bias goes into O
-        conv_fwd_sums(self.desc, D, W, O, ck, self.report, self.cap, self.workspace, faults, stream)
+        conv_fwd_sums(self.desc, D, W, O, ck, self.report, self.cap, self.workspace, faults, stream, given)
 
     def verify_correct_sums(self, D, W, O, stream=None, coc=False):
         """ftcnn_verify_correct_sums; coc=True also computes Co5..Co7 in the same launch."""

@@ -57,7 +57,7 @@ EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ft
            "ftcnn_encode", "ftcnn_conv_fwd", "ftcnn_checksum_conv", "ftcnn_verify", "ftcnn_correct",
            "ftcnn_verify_correct", "ftcnn_conv_fwd_ws", "ftcnn_conv_fwd_sums", "ftcnn_verify_correct_sums", "ftcnn_protected_conv",
            "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias", "ftcnn_check_weights",
-           "ftcnn_relu_pool")
+           "ftcnn_relu_pool", "ftcnn_relu_pool_encode", "ftcnn_conv_fwd_sums_given")
 
 _lib = None
 
@@ -97,6 +97,8 @@ def load(path: str = LIB_PATH):
     L.ftcnn_check_weights.restype = C.c_int
     L.ftcnn_relu_pool.argtypes = [C.c_int32] * 7 + [_dp, _dp, _dp]
     L.ftcnn_relu_pool.restype = C.c_int
+    L.ftcnn_relu_pool_encode.argtypes = [C.c_int32] * 8 + [_dp, _dp, _dp, _dp, _dp]
+    L.ftcnn_relu_pool_encode.restype = C.c_int
     L.ftcnn_conv_fwd_bias.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp, _dp]
     L.ftcnn_conv_fwd_bias.restype = C.c_int
     L.ftcnn_conv_fwd_ws.argtypes = [P(ConvDesc), _dp, _dp, _dp, _dp, _dp]
@@ -104,6 +106,8 @@ def load(path: str = LIB_PATH):
     L.ftcnn_conv_fwd_sums.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), _dp, C.c_int32, P(Fault),
                                       C.c_int32, _dp, _dp]
     L.ftcnn_conv_fwd_sums.restype = C.c_int
+    L.ftcnn_conv_fwd_sums_given.argtypes = L.ftcnn_conv_fwd_sums.argtypes
+    L.ftcnn_conv_fwd_sums_given.restype = C.c_int
     L.ftcnn_verify_correct_sums.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp,
                                             C.c_uint32, _dp, _dp]
     L.ftcnn_verify_correct_sums.restype = C.c_int

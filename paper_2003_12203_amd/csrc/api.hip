@@ -299,8 +299,11 @@ int check_faults(const Geom &g, const ftcnn_fault *faults, int nf, const char *w
 }
 
 int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
-                 ftcnn_report *rep, int32_t cap, const ftcnn_fault *faults, int32_t nf, void *ws, hipStream_t st) {
+                 ftcnn_report *rep, int32_t cap, const ftcnn_fault *faults, int32_t nf, void *ws, hipStream_t st,
+                 bool cd_given = false) {
     if (!D || !W || !O || !rep) return fail(FTCNN_E_ARG, "conv_fwd_sums: null pointer");
+    if (cd_given && (!ck || !ck->cd1 || !ck->cd2))
+        return fail(FTCNN_E_ARG, "conv_fwd_sums_given: ck->cd1 and ck->cd2 hold the given checksums");
     if (cap < 0) return fail(FTCNN_E_ARG, "negative cap_fixes");
     const double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
     if ((cd1 == nullptr) != (cd2 == nullptr)) return fail(FTCNN_E_ARG, "conv_fwd_sums: cd1 and cd2 go together");
@@ -309,7 +312,7 @@ int do_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ft
     FT_TRY(check_faults(pl.g, faults, nf, "conv_fwd_sums"));
     FT_TRY(check_ws(pl, ws));
     FT_TRY(weights_for_conv(pl, W, ws, st, &W));
-    FT_HIP(launch_conv_sums(pl, D, W, O, ck, rep, cap, faults, nf, ws, st), "conv_fwd_sums");
+    FT_HIP(launch_conv_sums(pl, D, W, O, ck, rep, cap, faults, nf, ws, st, cd_given), "conv_fwd_sums");
     return FTCNN_OK;
 }
 
@@ -349,6 +352,27 @@ KernelEvents &kernel_events() { return g_events; }
 }  // namespace ftcnn
 
 using namespace ftcnn;
+
+// Arguments of the operations between layers (ftcnn_relu_pool and its encoding form).
+int check_link(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s, const void *X,
+               const void *Y, const char *what) {
+    if (dtype != FTCNN_F32 && dtype != FTCNN_BF16) return fail(FTCNN_E_DTYPE, "%s: dtype %d", what, dtype);
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return fail(FTCNN_E_SHAPE, "%s: non-positive dimension", what);
+    if (!((k == 1 && s == 1) || (k == 2 && s == 2) || (k == 3 && s == 2)))
+        return fail(FTCNN_E_UNSUPPORTED, "%s: window %d stride %d (1/1, 2/2 and 3/2 are built)", what, k, s);
+    if (h < k || w < k) return fail(FTCNN_E_SHAPE, "%s: %dx%d map smaller than the %dx%d window", what, h, w, k, k);
+    if ((long long)n * c * h * w > (1LL << 40)) return fail(FTCNN_E_SHAPE, "%s: tensor too large", what);
+    if (!X || !Y) return fail(FTCNN_E_ARG, "%s: null pointer", what);
+    if (k > 1) {
+        // pooling reads windows of X while writing Y: the two must not overlap
+        const long long es = dtype == FTCNN_F32 ? 4 : 2;
+        const char *x0 = static_cast<const char *>(X), *y0 = static_cast<const char *>(Y);
+        const long long xb = (long long)n * c * h * w * es;
+        const long long yb = (long long)n * c * ((h - k) / s + 1) * ((w - k) / s + 1) * es;
+        if (x0 < y0 + yb && y0 < x0 + xb) return fail(FTCNN_E_ARG, "%s: X and Y overlap", what);
+    }
+    return FTCNN_OK;
+}
 
 extern "C" {
 
@@ -474,6 +498,14 @@ int ftcnn_conv_fwd_sums(const ftcnn_conv_desc *desc, const void *D, const void *
     return do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, faults, nf, workspace, stream);
 }
 
+int ftcnn_conv_fwd_sums_given(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                              const ftcnn_checksums *ck, ftcnn_report *rep, int32_t cap_fixes,
+                              const ftcnn_fault *faults, int32_t nf, void *workspace, hipStream_t stream) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    return do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, faults, nf, workspace, stream, true);
+}
+
 int ftcnn_verify_correct_sums(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                               const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                               uint32_t which, void *workspace, hipStream_t stream) {
@@ -503,22 +535,20 @@ int ftcnn_inject(const ftcnn_conv_desc *desc, void *O, const ftcnn_fault *faults
 
 int ftcnn_relu_pool(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s, const void *X,
                     void *Y, hipStream_t stream) {
-    if (dtype != FTCNN_F32 && dtype != FTCNN_BF16) return fail(FTCNN_E_DTYPE, "relu_pool: dtype %d", dtype);
-    if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return fail(FTCNN_E_SHAPE, "relu_pool: non-positive dimension");
-    if (!((k == 1 && s == 1) || (k == 2 && s == 2) || (k == 3 && s == 2)))
-        return fail(FTCNN_E_UNSUPPORTED, "relu_pool: window %d stride %d (1/1, 2/2 and 3/2 are built)", k, s);
-    if (h < k || w < k) return fail(FTCNN_E_SHAPE, "relu_pool: %dx%d map smaller than the %dx%d window", h, w, k, k);
-    if ((long long)n * c * h * w > (1LL << 40)) return fail(FTCNN_E_SHAPE, "relu_pool: tensor too large");
-    if (!X || !Y) return fail(FTCNN_E_ARG, "relu_pool: null pointer");
-    if (k > 1) {
-        // pooling reads windows of X while writing Y: the two must not overlap
-        const long long es = dtype == FTCNN_F32 ? 4 : 2;
-        const char *x0 = static_cast<const char *>(X), *y0 = static_cast<const char *>(Y);
-        const long long xb = (long long)n * c * h * w * es;
-        const long long yb = (long long)n * c * ((h - k) / s + 1) * ((w - k) / s + 1) * es;
-        if (x0 < y0 + yb && y0 < x0 + xb) return fail(FTCNN_E_ARG, "relu_pool: X and Y overlap");
-    }
+    const int rc = check_link(dtype, n, c, h, w, k, s, X, Y, "relu_pool");
+    if (rc != FTCNN_OK) return rc;
     FT_HIP(launch_relu_pool((ftcnn_dtype)dtype, X, Y, n, c, h, w, k, s, stream), "relu_pool");
+    return FTCNN_OK;
+}
+
+int ftcnn_relu_pool_encode(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t k, int32_t s,
+                           int32_t wbase, const void *X, void *Y, double *cd1, double *cd2, hipStream_t stream) {
+    if (!cd1 || !cd2) return fail(FTCNN_E_ARG, "relu_pool_encode: null checksum pointer");
+    if (wbase != 0 && wbase != 1) return fail(FTCNN_E_ARG, "relu_pool_encode: wbase must be 0 or 1");
+    const int rc = check_link(dtype, n, c, h, w, k, s, X, Y, "relu_pool_encode");
+    if (rc != FTCNN_OK) return rc;
+    FT_HIP(launch_relu_pool_encode((ftcnn_dtype)dtype, X, Y, n, c, h, w, k, s, wbase, cd1, cd2, stream),
+           "relu_pool_encode");
     return FTCNN_OK;
 }
 

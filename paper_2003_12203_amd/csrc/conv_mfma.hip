@@ -1109,7 +1109,7 @@ void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes) {
 
 hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
                             ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
-                            hipStream_t st) {
+                            hipStream_t st, bool cd_given) {
     char *w = static_cast<char *>(ws);
     double *cd1 = ck ? ck->cd1 : nullptr, *cd2 = ck ? ck->cd2 : nullptr;
     const void *Dc = D, *Wc = W;
@@ -1117,13 +1117,15 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
     int aux_kind = 0, aux_blocks = 0, co_slices = 0;
     CdSrc src{cd1, cd2, 0, 1};
     if (pl.nhwc) {
-        // channels-last copies; the copy of D also encodes Cd1, Cd2 (if asked)
-        const hipError_t e = launch_prep(pl, D, W, cd1, cd2, ws, st);
+        // channels-last copies; the copy of D also encodes Cd1, Cd2 (if asked and not given)
+        const hipError_t e = cd_given ? launch_prep(pl, D, W, nullptr, nullptr, ws, st)
+                                      : launch_prep(pl, D, W, cd1, cd2, ws, st);
         if (e != hipSuccess) return e;
         Dc = w + pl.off_dt;
         Wc = w + pl.off_wt;
         if (cd1) {
-            const int ns = pl.prep_ns;
+            // given checksums are whole: no image-range partials to combine
+            const int ns = cd_given ? 1 : pl.prep_ns;
             if (ns > 1) {
                 const double *p1 = reinterpret_cast<const double *>(w + pl.off_encp);
                 src = CdSrc{p1, p1 + pl.g.CHW, 2 * pl.g.CHW, ns};
@@ -1134,11 +1136,11 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
             aux_kind = aux_blocks > 0 ? 2 : 0;
             co_slices = coc ? pl.co.groups * ns : 0;
         }
-    } else if (cd1) {
+    } else if (cd1 && !cd_given) {
         aux_kind = 1;   // encode workgroups; their count follows the tile's threads
     }
     CocTile co = pl.co;
-    if (!(pl.nhwc && pl.prep_ns > 1)) co.comb_blocks = 0;
+    if (!(pl.nhwc && pl.prep_ns > 1) || cd_given) co.comb_blocks = 0;
     double *part = reinterpret_cast<double *>(w + pl.off_sums);
     double *copart = reinterpret_cast<double *>(w + pl.off_copart);
     const double *cw1 = ck ? ck->cw1 : nullptr, *cw2 = ck ? ck->cw2 : nullptr;

@@ -159,6 +159,9 @@ const void *dense_weights(const Plan &pl, const void *W, void *ws, hipStream_t s
 // ReLU then k x k / s max pooling between two layers of a network (k = s = 1: ReLU only)
 hipError_t launch_relu_pool(ftcnn_dtype dt, const void *X, void *Y, int n, int c, int h, int w, int k, int s,
                             hipStream_t st);
+// ... and the next layer's Cd1, Cd2 [c][h'][w'] from the values written
+hipError_t launch_relu_pool_encode(ftcnn_dtype dt, const void *X, void *Y, int n, int c, int h, int w, int k, int s,
+                                   int wbase, double *cd1, double *cd2, hipStream_t st);
 // Re-encode Cw1, Cw2 of W into the workspace (pl.off_wchk) and count the columns whose Cw1
 // differs bitwise from cw1 into *mismatches (Sec. 4.1.2).
 hipError_t launch_check_weights(const Plan &pl, const void *W, const double *cw1, int32_t *mismatches, void *ws,
@@ -177,7 +180,7 @@ hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, doubl
 // values before they are summed.
 hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
                             ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
-                            hipStream_t st);
+                            hipStream_t st, bool cd_given = false);
 // Rows of C per workgroup tile of the convolution chosen for this layer.
 int conv_tile_m(const Geom &g);
 // Threads per workgroup and dynamic LDS bytes of the convolution chosen for this layer.

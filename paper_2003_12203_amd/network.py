@@ -5,9 +5,12 @@ networks of Sec. 6): layer l + 1 receives ReLU and max pooling of layer l's outp
 layer l's correction, and encodes its Cd1, Cd2 from exactly that input.  Everything runs
 in the library's kernels on one stream:
 
-    per layer: ftcnn_conv_fwd_sums (channels-last copy + encode, convolution + sums)
+    per layer: ftcnn_conv_fwd_sums_given (channels-last copy, convolution + sums)
                ftcnn_verify_correct_sums (Co5..Co7, CoC-D, the correction chain)
-               ftcnn_relu_pool into the next layer's input
+               ftcnn_relu_pool_encode into the next layer's input and its Cd1, Cd2
+
+(the first layer encodes its own input in ftcnn_conv_fwd_sums' copy).  The next layer's
+checksums are thus encoded in the pass that writes its input, from the corrected values.
 
 and nothing waits on the host between layers.  Recomputation (Sec. 4.1.1) is the one
 decision the host takes: after the pass, the reports are read once, and from the first
@@ -45,9 +48,13 @@ class Chain:
     agree on the batch and on channels (m of layer l = ch of layer l + 1)."""
 
     def __init__(self, specs: Sequence[Tuple[int, ...]], dtype: str = "f32", policy=None,
-                 device: str = "cuda"):
+                 device: str = "cuda", fuse_encode: bool = True):
         if not specs:
             raise FtcnnError("a chain needs at least one layer")
+        # fuse_encode: the link between layers (ReLU, pooling) also encodes the next layer's
+        # Cd1, Cd2 from the values it writes (ftcnn_relu_pool_encode), and that layer takes them
+        # as given (ftcnn_conv_fwd_sums_given); otherwise each layer encodes in its own copy
+        self.fuse_encode = fuse_encode
         self.policy = policy or make_policy()
         self.layers: List[Layer] = [Layer(*sp, dtype=dtype, policy=self.policy, device=device) for sp in specs]
         self.links: List[Tuple[int, int]] = []
@@ -88,19 +95,28 @@ class Chain:
         return D0 if l == 0 else self.inputs[l]
 
     def launch(self, D0: torch.Tensor, faults: Optional[Sequence[Sequence[dict]]] = None, start: int = 0,
-               stream=None):
+               stream=None, linked: bool = False):
         """Enqueue the protected layers start.. on the stream (no host wait).  faults[l] (testing)
-        are planted in layer l's outputs before they are summed."""
+        are planted in layer l's outputs before they are summed.  linked: layer start's input (and,
+        with fuse_encode, its Cd1, Cd2) was just written by the link from layer start - 1."""
         if tuple(D0.shape) != self.layers[0].shape_d or D0.dtype != self.layers[0].tdtype:
             raise FtcnnError(f"input must be {self.layers[0].shape_d} {self.layers[0].tdtype}")
         if any(W is None for W in self.W):
             raise FtcnnError("set_weights first")
         for l in range(start, len(self.layers)):
             lay, D, O = self.layers[l], self._input(l, D0), self.outputs[l]
-            lay.conv_sums(D, self.W[l], O, faults[l] if faults else (), stream, encode=True)
+            # with fuse_encode, a layer after the first gets its Cd1, Cd2 from the pass that wrote
+            # its input (below); the first layer, and a restart, encode in the channels-last copy
+            given = self.fuse_encode and (l > start or (linked and l > 0))
+            lay.conv_sums(D, self.W[l], O, faults[l] if faults else (), stream, encode=not given, given=given)
             lay.verify_correct_sums(D, self.W[l], O, stream, coc=True)
             if l + 1 < len(self.layers):
-                relu_pool(O, *self.links[l], Y=self.inputs[l + 1], stream=stream)
+                self._link(l, O, stream)
+
+    def _link(self, l: int, O: torch.Tensor, stream=None):
+        nxt = self.layers[l + 1]
+        cd = (nxt.buf["cd1"], nxt.buf["cd2"]) if self.fuse_encode else None
+        relu_pool(O, *self.links[l], Y=self.inputs[l + 1], stream=stream, cd=cd, wbase=nxt.desc.wbase)
 
     def launch_plain(self, D0: torch.Tensor, stream=None):
         """The same network unprotected: the same convolution kernels with no ABFT work, and the
@@ -141,8 +157,8 @@ class Chain:
             again = lay.read_report()
             rep.status = STATUS_FAILED if again.detected else STATUS_RECOMPUTED
             if l + 1 < len(self.layers):
-                relu_pool(O, *self.links[l], Y=self.inputs[l + 1], stream=stream)
-                self.launch(D0, None, l + 1, stream)
+                self._link(l, O, stream)
+                self.launch(D0, None, l + 1, stream, linked=True)
                 for j in range(l + 1, len(self.layers)):
                     reps[j] = self.layers[j].read_report()
         return reps

@@ -124,6 +124,22 @@ def test_relu_pool_rejects_bad_arguments_without_launch():
     assert L.ftcnn_relu_pool(ft.F32, 2, 3, 8, 8, 2, 2, X, C.c_void_p((1 << 20) + 4 * 2 * 3 * 64 - 4), None) == -1
 
 
+def test_relu_pool_encode_rejects_bad_arguments_without_launch():
+    L = _lib.load()
+    X, Y, c = C.c_void_p(1 << 20), C.c_void_p(1 << 24), C.c_void_p(1 << 28)
+    assert L.ftcnn_relu_pool_encode(ft.F32, 2, 3, 8, 8, 2, 2, 0, X, Y, None, c, None) == -1
+    assert L.ftcnn_relu_pool_encode(ft.F32, 2, 3, 8, 8, 2, 2, 2, X, Y, c, c, None) == -1     # wbase
+    assert L.ftcnn_relu_pool_encode(ft.F32, 2, 3, 8, 8, 3, 1, 0, X, Y, c, c, None) == -6
+    assert L.ftcnn_relu_pool_encode(ft.F32, 2, 3, 8, 8, 2, 2, 0, X, X, c, c, None) == -1     # overlap
+    d = ft.make_desc(2, 32, 8, 8, 16, 3, 3, 1, 1)
+    ck = _lib.Checksums()
+    rep = C.c_void_p(256)
+    # the given checksums are required
+    assert L.ftcnn_conv_fwd_sums_given(C.byref(d), X, X, Y, C.byref(ck), rep, 4, None, 0, C.c_void_p(256),
+                                       None) == -1
+    assert L.ftcnn_conv_fwd_sums_given(C.byref(d), X, X, Y, None, rep, 4, None, 0, C.c_void_p(256), None) == -1
+
+
 def test_chain_shapes_checked_on_host():
     from paper_2003_12203_amd import network
     assert network.pooling(55, 27) == (3, 2) and network.pooling(224, 112) == (2, 2)

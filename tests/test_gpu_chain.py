@@ -3,9 +3,13 @@ oracle's chain.
 
 * ftcnn_relu_pool equals the oracle's ReLU + max pooling bit for bit (fp32 and bf16; 1x1, 2x2/2,
   3x3/2; odd sizes; negative values, signed zeros, NaN; ReLU in place);
+* ftcnn_relu_pool_encode: the same values, and the next layer's Cd1, Cd2 equal to the oracle's
+  encode of them (wbase 0 and 1; in place for ReLU alone);
 * a three-layer chain on integer data (fp32, every value exact): with a fault planted in every
-  layer each layer's fixes are the oracle's, each layer's input is the oracle's, and the output is
-  the fault-free chain's bit for bit; the AlexNet-style 3x3/2 pooling chain as well;
+  layer each layer's fixes are the oracle's, each layer's input and Cd1 are the oracle's, and the
+  output is the fault-free chain's bit for bit; the AlexNet-style 3x3/2 pooling chain as well;
+  with the next layer's checksums encoded by the link (ftcnn_conv_fwd_sums_given) and by each
+  layer's own copy;
 * a bf16 chain (channels-last layers) within the bf16 tolerance, fixes equal to the oracle's;
 * a layer beyond every scheme is recomputed and the layers after it run again on its clean output.
 """
@@ -43,6 +47,32 @@ def test_relu_pool_matches_oracle(dt, k, s, h, w):
         assert torch.equal(X.view(iv), Y.view(iv))
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("k,s,h,w", [(1, 1, 7, 9), (1, 1, 16, 16), (2, 2, 11, 13), (3, 2, 27, 27)])
+@pytest.mark.parametrize("wbase", [0, 1])
+def test_relu_pool_encode_matches_oracle(dt, k, s, h, w, wbase):
+    g = np.random.default_rng([12203, 94, k, h, w])
+    x = g.normal(size=(6, 5, h, w)).astype(np.float32)
+    x.flat[5::31] = np.nan
+    X = dev(x, dt)
+    ref = och.link(host(X), k, s)
+    cd1 = torch.zeros(ref[0].size, dtype=torch.float64, device="cuda")
+    cd2 = torch.zeros_like(cd1)
+    print(f"[relu_pool_encode] {dt} k={k} s={s} {h}x{w} wbase={wbase}", flush=True)
+    Y = ft.relu_pool(X, k, s, cd=(cd1, cd2), wbase=wbase)
+    np.testing.assert_array_equal(host(Y), ref)
+    r1, r2 = wf.encode(ref, wbase)
+    np.testing.assert_allclose(cd1.cpu().numpy(), r1.ravel(), rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(cd2.cpu().numpy(), r2.ravel(), rtol=1e-13, atol=1e-12)
+    if k == 1:   # in place, the same values and checksums
+        c1 = torch.zeros_like(cd1)
+        c2 = torch.zeros_like(cd1)
+        X2 = dev(x, dt)
+        ft.relu_pool(X2, 1, 1, Y=X2, cd=(c1, c2), wbase=wbase)
+        iv = torch.int16 if dt == "bf16" else torch.int32
+        assert torch.equal(X2.view(iv), Y.view(iv)) and torch.equal(c1, cd1) and torch.equal(c2, cd2)
+
+
 def _specs(n, chs, hs, rs, pads):
     return [(n, chs[l], hs[l], hs[l], chs[l + 1], rs[l], rs[l], 1, pads[l]) for l in range(len(rs))]
 
@@ -78,11 +108,12 @@ CHAINS = [
 ]
 
 
+@pytest.mark.parametrize("fuse", [True, False], ids=["link-encode", "copy-encode"])
 @pytest.mark.parametrize("case", CHAINS, ids=lambda c: f"{c[0]}-{'-'.join(map(str, c[1]))}-{c[5]}")
-def test_chain_integer_matches_oracle(case):
+def test_chain_integer_matches_oracle(case, fuse):
     n, chs, hs, rs, pads, dt = case
     specs = _specs(n, chs, hs, rs, pads)
-    net = network.Chain(specs, dt)
+    net = network.Chain(specs, dt, fuse_encode=fuse)
     Ws = _weights(chs, rs, sum(chs), True, dt)
     D0 = np.random.default_rng([12203, 97, n]).integers(0, 3, size=(n, chs[0], hs[0], hs[0])).astype(np.float64)
     net.set_weights([dev(W, dt) for W in Ws])
