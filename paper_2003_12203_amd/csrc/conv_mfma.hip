@@ -1054,7 +1054,7 @@ long long n_tiles(const Geom &g, int tm, int tp) {
 
 using F32_M32 = Tile<F32T<16>, 1, 4, 1, 2, true>;
 using F32_M64 = Tile<F32T<16>, 2, 2, 1, 2, true>;
-using F32_M96 = Tile<F32T<16>, 1, 4, 3, 2, true>;
+using F32_M96 = Tile<F32T<16>, 1, 4, 3, 1, true>;   // 96 x 128: AlexNet conv1 gets 1513 tiles, 3 full rounds
 using F32_128x128 = Tile<F32T<16>, 2, 2, 2, 2, true>;
 using F32_128x64 = Tile<F32T<32>, 2, 2, 2, 1, true>;
 using F32_64x64 = Tile<F32T<32>, 2, 2, 1, 1, true>;
