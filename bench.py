@@ -381,7 +381,12 @@ def chain_bench(args, cfg, runs, ft, torch):
         sys.exit(2)
     specs = [(l.n, l.ch, l.h, l.w, l.m, l.r, l.s, l.stride, l.pad) for l in cfg.layers]
     dtype = cfg.layers[0].dtype
-    net = network.Chain(specs, dtype)
+    try:
+        net = network.Chain(specs, dtype)
+    except ft.FtcnnError as e:
+        print(f"bench.py: the {cfg.name} layers do not form a chain ({e}); --chain runs AlexNet, VGG-19 "
+              "and Darknet-19", file=sys.stderr)
+        sys.exit(2)
     net.set_weights([r.W for r in runs])
     D0 = runs[0].D
     nl = len(runs)
