@@ -632,10 +632,30 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     Pack<T, C::VEC> ra[C::A_PER];
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
+    // grouped layers (Sec. 5.2) run on the block-diagonal expansion of W: a tile whose filters all
+    // lie in one group needs only the chunks of K = (r, s, c) with c in that group's channels (the
+    // others multiply zeros), and the channels-last loop below walks just those
+    constexpr bool KSKIP = NHWC && !DMA && WEAVE != 2;
+    int nch = nchunks, cpr = 0, cg0 = 0;
+    if constexpr (KSKIP) {
+        const int mlast = (m0 + C::TM < g.M ? m0 + C::TM : g.M) - 1;
+        if (g.G > 1 && g.Cg % C::TK == 0 && m0 / g.Mg == mlast / g.Mg) {
+            cpr = g.Cg / C::TK;
+            cg0 = group_first_channel(g, m0);
+            nch = g.R * g.S * cpr;
+        }
+    }
+    auto kbase = [&](int j) {
+        if (KSKIP && cpr > 0) {
+            const int rs = j / cpr;
+            return rs * g.C + cg0 + (j - rs * cpr) * C::TK;
+        }
+        return j * C::TK;
+    };
     typename C::Mask amask = 0, bmask = 0;
     if constexpr (!DMA) {
-        amask = load_a<C>(Wt, g, 0, KVEC, as, ra);
-        bmask = NHWC ? load_b_nhwc<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
+        amask = load_a<C>(Wt, g, kbase(0), KVEC, as, ra);
+        bmask = NHWC ? load_b_nhwc<C>(D, g, kbase(0) + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
                      : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
         store_lds<C, NHWC>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
         __syncthreads();
@@ -674,9 +694,9 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     } else if constexpr (NHWC) {
         // channels-last: a whole chunk's gather is a few 16-byte loads per thread, issued
         // before this chunk's MFMAs and stored after them
-        for (int kc = 0; kc + 1 < nchunks; ++kc) {
+        for (int kc = 0; kc + 1 < nch; ++kc) {
             const int buf = kc & 1;
-            const int kb = (kc + 1) * C::TK;
+            const int kb = kbase(kc + 1);
             amask = load_a<C>(Wt, g, kb, KVEC, as, ra);
             bmask = load_b_nhwc<C>(D, g, kb + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
             mma_chunk<C, FM, FP>(As0 + buf * C::TM * C::LDK, Bs0 + buf * C::TP * C::LDK, lane, arow0, brow0, acc);
@@ -684,7 +704,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                          bmask, bp, bkg);
             __syncthreads();
         }
-        mma_chunk<C, FM, FP>(As0 + ((nchunks - 1) & 1) * C::TM * C::LDK, Bs0 + ((nchunks - 1) & 1) * C::TP * C::LDK,
+        mma_chunk<C, FM, FP>(As0 + ((nch - 1) & 1) * C::TM * C::LDK, Bs0 + ((nch - 1) & 1) * C::TP * C::LDK,
                              lane, arow0, brow0, acc);
     } else if constexpr (WEAVE == 2 && sizeof(T) == 4) {
         // two chunks in flight: while a chunk is consumed from one LDS buffer, the gather of the
