@@ -1093,6 +1093,9 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
         if (g.M <= 32) return f(F32_M32{});
         if (g.M <= 64) return f(F32_M64{});
         if (g.M <= 96) return f(F32_M96{});
+        // grouped layers: rows of tiles inside one group, so that every tile skips the other
+        // groups' channels (192 filters a group: 64-row tiles)
+        if (g.G > 1 && g.Mg % 128 != 0 && g.Mg % 64 == 0) return f(F32_64x64{});
         if (n_tiles(g, 128, 128) >= 600) return f(F32_128x128{});
         if (n_tiles(g, 128, 64) >= 380) return f(F32_128x64{});
         return f(F32_64x64{});
