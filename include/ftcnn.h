@@ -252,8 +252,7 @@ int ftcnn_conv_fwd_ws(const ftcnn_conv_desc *desc, const void *D, const void *W,
 /* Eq. (1) as ftcnn_conv_fwd_ws (same kernels, bitwise the same O), with the
  * CoC-D summations of Sec. 3.6 computed in the epilogue from the values as
  * stored: every workgroup tile writes, for each of its output pixels, the
- * partial So5, So6 and sum of squares over its filters (So7's share is the
- * pixel's image weight times So5's) into the
+ * partial So5, So6, So7 and sum of squares over its filters into the
  * workspace, so detection never re-reads O.  Also resets *rep (cap_fixes
  * recorded).  Follow it with ftcnn_verify_correct_sums on the same workspace
  * and report.

@@ -106,7 +106,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     pl->off_ver = off;
     off += align256(4ull * pl->ver_splits * EF * sizeof(double));
     pl->off_sums = off;
-    off += align256(3ull * pl->sum_splits * EF * sizeof(double));
+    off += align256(4ull * pl->sum_splits * EF * sizeof(double));
     // channels-last copies of D and W for the vector-gather convolution; the copy of D encodes
     // Cd1, Cd2 too, over image ranges when the layer has few tiles: enough ranges for about 1024
     // workgroups, with at least 16 images (fp32) or 32 (bf16) a range, so that the float64 partial

@@ -921,10 +921,11 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                 if (h == 0 && cval[j]) {
                     const long long pgo = pcol[j];
                     const long long n = pgo / g.EF;
-                    double *dst = ep.part + ((size_t)mt * g.N + n) * 3 * g.EF + (pgo - n * g.EF);
+                    double *dst = ep.part + ((size_t)mt * g.N + n) * 4 * g.EF + (pgo - n * g.EF);
                     dst[0] = a1;
                     dst[g.EF] = a6;
-                    dst[2 * (size_t)g.EF] = aq;
+                    dst[2 * (size_t)g.EF] = ((double)n + wb) * a1;
+                    dst[3 * (size_t)g.EF] = aq;
                 }
             } else if (h == 0) {
                 red[(wm * 3 + 0) * C::TP + cl] = a1;
@@ -945,10 +946,11 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                     sq += red[(w * 3 + 2) * C::TP + cl];
                 }
                 const long long n = pgo / g.EF;
-                double *dst = ep.part + ((size_t)mt * g.N + n) * 3 * g.EF + (pgo - n * g.EF);
+                double *dst = ep.part + ((size_t)mt * g.N + n) * 4 * g.EF + (pgo - n * g.EF);
                 dst[0] = s1;
                 dst[g.EF] = s6;
-                dst[2 * (size_t)g.EF] = sq;
+                dst[2 * (size_t)g.EF] = ((double)n + wb) * s1;
+                dst[3 * (size_t)g.EF] = sq;
             }
         }
         if constexpr (EPI == 2) {
@@ -967,10 +969,11 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                         const typename Bt::B b = *o, b2 = fault_apply(b, q);
                         *o = b2;
                         const double v = (double)Bt::value(b), v2 = (double)Bt::value(b2), d = v2 - v;
-                        double *dst = ep.part + ((size_t)mt * g.N + q.n) * 3 * g.EF + pos;
+                        double *dst = ep.part + ((size_t)mt * g.N + q.n) * 4 * g.EF + pos;
                         dst[0] += d;
                         dst[g.EF] += ((double)q.m + wb) * d;
-                        dst[2 * (size_t)g.EF] += v2 * v2 - v * v;
+                        dst[2 * (size_t)g.EF] += ((double)q.n + wb) * d;
+                        dst[3 * (size_t)g.EF] += v2 * v2 - v * v;
                     }
                 }
             }

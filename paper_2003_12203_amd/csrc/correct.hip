@@ -752,7 +752,7 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
                                                                   double *co5, double *co6, double *co7,
                                                                   double *so5, double *so6, double *so7, double *q5,
                                                                   int *__restrict__ flags, double *scratch,
-                                                                  size_t stride, int nslots, int nimg) {
+                                                                  size_t stride, int nslots) {
     __shared__ Sh sh;
     constexpr int NV = COC ? 7 : 4;
     __shared__ double red[TPP > 1 ? NV : 1][TPP > 1 ? 4 * (kThreads / TPP) : 1];
@@ -771,19 +771,9 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int s = s0 + u * TPP;
-                const int sc = s < splits ? s : 0;
-                if (nimg > 0) {
-                    // [So5, So6, sum of squares] of image sc % nimg: So7's share is (n + wbase) So5
-                    const double *ps = part + (size_t)sc * 3 * g.EF + p;
-                    x[u][0] = ps[0];
-                    x[u][1] = ps[g.EF];
-                    x[u][3] = ps[2 * (size_t)g.EF];
-                    x[u][2] = ((double)(sc % nimg) + (double)c.wb) * x[u][0];
-                } else {
-                    const double *ps = part + (size_t)sc * 4 * g.EF + p;
+                const double *ps = part + (size_t)(s < splits ? s : 0) * 4 * g.EF + p;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) x[u][i] = ps[i * (size_t)g.EF];
-                }
+                for (int i = 0; i < 4; ++i) x[u][i] = ps[i * (size_t)g.EF];
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
@@ -934,7 +924,7 @@ Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftc
 template <typename T>
 hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums &ck,
                      const ftcnn_policy &pol, ftcnn_report *rep, void *ws, size_t off_part, int sp, bool coc,
-                     int nimg, hipStream_t st) {
+                     hipStream_t st) {
     const Ctx<T> c = make_ctx<T>(pl, D, W, O, ck, pol, rep);
     char *w = static_cast<char *>(ws);
     const double *part = reinterpret_cast<const double *>(w + off_part);
@@ -951,7 +941,7 @@ hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, cons
     verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, copart, max_groups, ck.co5,       \
                                                                     ck.co6, ck.co7,                              \
                                                                     ck.so5, ck.so6, ck.so7, ck.q5, flags,        \
-                                                                    scratch, pl.corr_stride, pl.corr_slots, nimg)
+                                                                    scratch, pl.corr_stride, pl.corr_slots)
     if (coc) {
         if (tpp == 1) VC(1, true);
         else if (tpp == 4) VC(4, true);
@@ -1013,16 +1003,16 @@ hipError_t launch_verify_correct(const Plan &pl, const void *D, const void *W, v
     hipError_t e = launch_verify_partial(pl, O, rep, cap, ws, st);
     if (e != hipSuccess) return e;
     if (pl.g.dtype == FTCNN_F32)
-        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, false, 0, st);
-    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, false, 0, st);
+        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, false, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_ver, pl.ver_splits, false, st);
 }
 
 hipError_t launch_verify_correct_sums(const Plan &pl, const void *D, const void *W, void *O,
                                       const ftcnn_checksums &ck, const ftcnn_policy &pol, ftcnn_report *rep,
                                       bool coc, void *ws, hipStream_t st) {
     if (pl.g.dtype == FTCNN_F32)
-        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, coc, pl.g.N, st);
-    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, coc, pl.g.N, st);
+        return run_fused<float>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, coc, st);
+    return run_fused<uint16_t>(pl, D, W, O, ck, pol, rep, ws, pl.off_sums, pl.sum_splits, coc, st);
 }
 
 }  // namespace ftcnn

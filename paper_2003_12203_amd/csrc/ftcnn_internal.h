@@ -169,9 +169,8 @@ hipError_t launch_check_weights(const Plan &pl, const void *W, const double *cw1
 // c1 = sum_m bias[m], c2 = sum_m (m + wbase) bias[m] (Sec. 5.1), one double each.
 hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, double *c2, hipStream_t st);
 // The convolution with the CoC-D summations in its epilogue: every tile also
-// writes its (So5, So6, sum of squares) partials for the pixels it owns to the
-// workspace (pl.sum_splits slices [tile row][image], the final launch derives
-// So7's share as (n + wbase) So5 from the slice's image) and
+// writes its (So5, So6, So7, sum of squares) partials for the pixels it owns to
+// the workspace (pl.sum_splits slices, layout of the verification partials) and
 // the report is reset.  With ck->cd1 and cd2 set, Cd1 and Cd2 are encoded in
 // the same pass (by the channels-last copy, or by extra workgroups of the
 // convolution launch); on pl.co_in_conv layers with ck->cw1 and cw2 set too,
