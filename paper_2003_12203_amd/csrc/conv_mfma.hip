@@ -552,7 +552,7 @@ template <> struct Bits<uint16_t> {
     __device__ static float value(B b) { return bf16_bits_to_f32(b); }
 };
 
-template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC, bool GRP = false>
 __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T *__restrict__ D,
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
@@ -635,7 +635,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     // grouped layers (Sec. 5.2) run on the block-diagonal expansion of W: a tile whose filters all
     // lie in one group needs only the chunks of K = (r, s, c) with c in that group's channels (the
     // others multiply zeros), and the channels-last loop below walks just those
-    constexpr bool KSKIP = NHWC && !DMA && WEAVE != 2;
+    constexpr bool KSKIP = GRP && NHWC && !DMA && WEAVE != 2;   // a separate kernel: dense loops unchanged
     int nch = nchunks, cpr = 0, cg0 = 0;
     if constexpr (KSKIP) {
         const int mlast = (m0 + C::TM < g.M ? m0 + C::TM : g.M) - 1;
@@ -981,7 +981,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     }
 }
 
-template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC, bool GRP = false>
 hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
                       const void *zp, const Epi<EPI> &ep) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
@@ -1013,7 +1013,7 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
         }
     }
     if (grid > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI, NHWC>;
+    auto kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI, NHWC, GRP>;
     if constexpr (C::LDS_BYTES > 65536) {
         static const hipError_t attr = hipFuncSetAttribute(
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
@@ -1051,6 +1051,10 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
             if (!nhwc || !zp) return hipErrorInvalidValue;
             return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
         } else {
+            if constexpr (WEAVE != 2) {
+                if (nhwc && g.G > 1)   // grouped: the loop that skips other groups' channels
+                    return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true, true>(g, D, W, O, st, 0, zp, ep);
+            }
             if (nhwc) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
             const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
             if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, false>(g, D, W, O, st, 0, zp, ep);
