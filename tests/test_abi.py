@@ -146,3 +146,18 @@ def test_chain_shapes_checked_on_host():
     assert network.pooling(13, 13) == (1, 1)
     with pytest.raises(ft.FtcnnError):
         network.pooling(8, 3)
+
+
+def test_chain_links_and_mismatches_on_host():
+    """network.Chain works out the operations between layers on the host (no device work): ReLU
+    alone for equal sizes, AlexNet's 3x3/2 and VGG's 2x2/2 pooling, and it rejects layers that do
+    not feed each other."""
+    from paper_2003_12203_amd import network
+    vgg = [(2, 3, 16, 16, 8, 3, 3, 1, 1), (2, 8, 16, 16, 8, 3, 3, 1, 1), (2, 8, 8, 8, 4, 3, 3, 1, 1)]
+    assert network.Chain(vgg, "f32", device="cpu").links == [(1, 1), (2, 2)]
+    alex = [(2, 3, 29, 29, 8, 5, 5, 2, 0), (2, 8, 6, 6, 4, 3, 3, 1, 1)]   # 13 -> 3x3/2 -> 6
+    assert network.Chain(alex, "f32", device="cpu").links == [(3, 2)]
+    with pytest.raises(ft.FtcnnError):   # 8 filters feed a layer of 6 channels
+        network.Chain([(2, 3, 16, 16, 8, 3, 3, 1, 1), (2, 6, 16, 16, 8, 3, 3, 1, 1)], "f32", device="cpu")
+    with pytest.raises(ft.FtcnnError):   # 16 -> 7: no 2x2/2 or 3x3/2 pooling fits exactly
+        network.Chain([(2, 3, 16, 16, 8, 3, 3, 1, 1), (2, 8, 7, 7, 8, 3, 3, 1, 1)], "f32", device="cpu")
