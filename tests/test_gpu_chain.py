@@ -11,7 +11,8 @@ oracle's chain.
   with the next layer's checksums encoded by the link (ftcnn_conv_fwd_sums_given) and by each
   layer's own copy;
 * a bf16 chain (channels-last layers) within the bf16 tolerance, fixes equal to the oracle's;
-* a layer beyond every scheme is recomputed and the layers after it run again on its clean output.
+* a layer beyond every scheme is recomputed and the layers after it run again on its clean output;
+* the encoding link at VGG-19's, AlexNet's and Darknet-19's full sizes, sampled: values and Cd.
 """
 import numpy as np
 import pytest
@@ -168,3 +169,32 @@ def test_chain_recomputes_and_runs_on():
     net.launch_plain(dev(D0, dt))
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(net.outputs[-1]), clean.output)
+
+
+@pytest.mark.parametrize("shape,k,s,dt", [((32, 64, 224, 224), 2, 2, "bf16"),    # VGG-19 after v2
+                                          ((64, 96, 55, 55), 3, 2, "f32"),        # AlexNet after conv1
+                                          ((16, 256, 52, 52), 1, 1, "f32")],      # Darknet-19 after c6
+                         ids=["vgg-v2-bf16", "alexnet-conv1", "darknet-c6"])
+def test_link_encode_full_size_sampled(shape, k, s, dt):
+    """The encoding link at the networks' full sizes, in the launch the chained bench times: every
+    output value and the next layer's Cd1, Cd2 at 256 sampled positions against the oracle's
+    ReLU, pooling and encode of the same windows."""
+    n, c, h, w = shape
+    g = torch.Generator(device="cuda").manual_seed(12203)
+    X = torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16 if dt == "bf16" else torch.float32)
+    Ho, Wo = (h - k) // s + 1, (w - k) // s + 1
+    cd1 = torch.empty(c * Ho * Wo, dtype=torch.float64, device="cuda")
+    cd2 = torch.empty_like(cd1)
+    print(f"[link full] {shape} {k}/{s} {dt}", flush=True)
+    Y = ft.relu_pool(X, k, s, cd=(cd1, cd2))
+    torch.cuda.synchronize()
+    r = np.random.default_rng([12203, 99, c])
+    cs, is_, js = r.integers(0, c, 256), r.integers(0, Ho, 256), r.integers(0, Wo, 256)
+    for cc, i, j in zip(cs, is_, js):
+        win = host(X[:, cc:cc + 1, s * i:s * i + k, s * j:s * j + k].contiguous())   # [N][1][k][k]
+        ref = och.link(win, k, s)[:, 0, 0, 0]
+        np.testing.assert_array_equal(host(Y[:, cc, i, j]), ref)
+        r1, r2 = wf.encode(ref[:, None], 0)
+        o = (cc * Ho + i) * Wo + j
+        np.testing.assert_allclose(cd1[o].item(), r1[0], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(cd2[o].item(), r2[0], rtol=1e-13, atol=1e-11)
