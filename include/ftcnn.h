@@ -18,8 +18,9 @@
  *   library never allocates, frees or retains device memory; scratch comes
  *   from a caller-supplied workspace of ftcnn_workspace_bytes() bytes
  *   (256-byte aligned).
- * - Layouts are dense row-major: D [n][ch][h][w], W [m][ch][r][s],
- *   O [n][m][E][F] with E = floor((h + 2*pad - r)/stride) + 1 and
+ * - Layouts are dense row-major: D [n][ch][h][w], W [m][ch/groups][r][s]
+ *   (W [m][ch][r][s] when groups = 1), O [n][m][E][F] with
+ *   E = floor((h + 2*pad - r)/stride) + 1 and
  *   F = floor((w + 2*pad - s)/stride) + 1.  D, W and O share the dtype of the
  *   descriptor (fp32, or bf16 as raw 16-bit patterns); accumulation is fp32 in
  *   the convolution and fp64 everywhere on the checksum side, except that a
@@ -57,7 +58,9 @@ enum {
     FTCNN_E_DTYPE = -3,        /* dtype not FTCNN_F32 / FTCNN_BF16               */
     FTCNN_E_WORKSPACE = -4,    /* workspace missing or misaligned                */
     FTCNN_E_HIP = -5,          /* kernel launch failed                           */
-    FTCNN_E_UNSUPPORTED = -6   /* e.g. groups != 1                               */
+    FTCNN_E_UNSUPPORTED = -6   /* a combination that is not built, e.g. a grouped
+                                  layer without a workspace, a pooling window
+                                  other than 1/1, 2/2 and 3/2                     */
 };
 
 typedef enum { FTCNN_F32 = 0, FTCNN_BF16 = 1 } ftcnn_dtype;
@@ -65,9 +68,15 @@ typedef enum { FTCNN_F32 = 0, FTCNN_BF16 = 1 } ftcnn_dtype;
 /* One convolution layer (notation of Sec. 2.1, Table 1: N, Ch, H, M, R, U). */
 typedef struct {
     int32_t n, ch, h, w;     /* D [n][ch][h][w]                                  */
-    int32_t m, r, s;         /* W [m][ch][r][s]                                  */
+    int32_t m, r, s;         /* W [m][ch/groups][r][s]                           */
     int32_t stride, pad;     /* U of eq. (1); zero padding on every side         */
-    int32_t groups;          /* must be 1                                        */
+    int32_t groups;          /* G >= 1 dividing ch and m (Sec. 5.2): filter m
+                                sees channels [(m / (m_total/G)) * ch/G, + ch/G).
+                                G > 1 needs the workspace in every call that
+                                reads W (the convolution runs on the
+                                block-diagonal expansion of W kept there):
+                                ftcnn_conv_fwd and Co1/Co3 of
+                                ftcnn_checksum_conv return FTCNN_E_UNSUPPORTED */
     int32_t dtype;           /* ftcnn_dtype of D, W and O                        */
     int32_t wbase;           /* block index weight offset, 0 or 1                */
 } ftcnn_conv_desc;
@@ -164,6 +173,18 @@ size_t ftcnn_report_bytes(int32_t cap_fixes);
 
 /* Description of the last error on the calling thread ("" if none). */
 const char *ftcnn_last_error(void);
+
+/* INSTRUMENTATION (host-only, no device work; not an operation of the paper): the
+ * convolution kernel this layer's calls launch.  path 0: ftcnn_conv_fwd and
+ * ftcnn_conv_fwd_bias without a workspace (D and W read as given); path 1: every call
+ * that takes a workspace (ftcnn_conv_fwd_ws, ftcnn_conv_fwd_sums, ftcnn_protected_conv,
+ * ...).  out[0] = filters (rows of W) per workgroup tile, out[1] = output pixels per tile,
+ * out[2] = k per LDS chunk, out[3] = main loop (0 register-staged gather, 1 gather woven
+ * between the matrix-core instructions, 2 two chunks in flight, 3 direct-to-LDS loads),
+ * out[4] = 1 when the convolution reads channels-last copies, out[5] = 1 when its tiles
+ * skip the channels of other groups (grouped layers).  Lets a test check that it covers
+ * every kernel a set of layers runs. */
+int ftcnn_conv_tile(const ftcnn_conv_desc *desc, int32_t path, int32_t out[6]);
 
 /* ---- device work -------------------------------------------------------- */
 

@@ -78,6 +78,14 @@ def report_bytes(cap: int) -> int:
     return int(lib().ftcnn_report_bytes(cap))
 
 
+def conv_tile(desc, path: int = 1) -> dict:
+    """ftcnn_conv_tile: the convolution kernel a layer's calls launch (host-only query)."""
+    out = (C.c_int32 * 6)()
+    _check(lib().ftcnn_conv_tile(C.byref(desc), int(path), out), "ftcnn_conv_tile")
+    return {"tm": out[0], "tp": out[1], "tk": out[2], "loop": out[3], "nhwc": bool(out[4]),
+            "group_skip": bool(out[5])}
+
+
 def last_error() -> str:
     return lib().ftcnn_last_error().decode(errors="replace")
 

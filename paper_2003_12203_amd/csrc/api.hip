@@ -38,7 +38,9 @@ int row_splits(long long rows, long long col_blocks, long long target_blocks, lo
     return clampi(want, 1, cap);
 }
 
-int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
+// allow_nhwc = false: every convolution gathers from D as given (no channels-last copies in
+// the workspace), a plan with a smaller workspace for layers that would otherwise copy.
+int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
     if (!d) return fail(FTCNN_E_ARG, "null descriptor");
     if (d->groups < 1 || d->ch % d->groups != 0 || d->m % d->groups != 0)
         return fail(FTCNN_E_SHAPE, "groups = %d must divide ch = %d and m = %d", d->groups, d->ch, d->m);
@@ -87,8 +89,9 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     const long long part_cap = part_budget / (32 * EF);
     pl->ver_splits = row_splits(rows_o, ceil_div(cols_v, ctt), 1024, 32);
     if (pl->ver_splits > part_cap) pl->ver_splits = part_cap > 1 ? (int)part_cap : 1;
+    pl->nhwc = allow_nhwc && nhwc_layer(g);
     // summations fused into the convolution epilogue: one slice per (filter tile, image)
-    pl->sum_splits = (int)(ceil_div(g.M, conv_tile_m(g)) * g.N);
+    pl->sum_splits = (int)(ceil_div(g.M, conv_tile_m(g, pl->nhwc)) * g.N);
     // correction: the standalone launch has corr_blocks workgroups, one scratch slice each; in
     // the fused final stage a workgroup with flagged positions takes the next free slice
     pl->corr_blocks = 256;
@@ -111,7 +114,6 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
     // Cd1, Cd2 too, over image ranges when the layer has few tiles: enough ranges for about 1024
     // workgroups, with at least 16 images (fp32) or 32 (bf16) a range, so that the float64 partial
     // pairs (16 bytes per element of Cd) cost at most a quarter of D's traffic, and at most 16
-    pl->nhwc = nhwc_layer(g);
     const size_t es = g.dtype == FTCNN_F32 ? 4 : 2;
     pl->prep_ns = 1;
     pl->co_in_conv = false;
@@ -129,7 +131,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl) {
         // final launch evaluates the taps itself.
         int nt = 0;
         size_t lds = 0;
-        conv_tile_shape(g, &nt, &lds);
+        conv_tile_shape(g, true, &nt, &lds);
         CocTile &co = pl->co;
         co.tx = g.F >= 24 ? 32 : (g.F >= 12 ? 16 : 8);
         co.ty = nt / co.tx < g.E ? nt / co.tx : g.E;
@@ -396,6 +398,17 @@ size_t ftcnn_workspace_bytes(const ftcnn_conv_desc *desc) {
     Plan pl;
     if (make_plan(desc, &pl) != FTCNN_OK) return 0;
     return pl.bytes;
+}
+
+int ftcnn_conv_tile(const ftcnn_conv_desc *desc, int32_t path, int32_t out[6]) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (!out) return fail(FTCNN_E_ARG, "conv_tile: null output");
+    if (path != 0 && path != 1) return fail(FTCNN_E_ARG, "conv_tile: path %d (0 or 1)", path);
+    int o[6];
+    conv_tile_info(pl.g, path == 1 && pl.nhwc, o);
+    for (int i = 0; i < 6; ++i) out[i] = o[i];
+    return FTCNN_OK;
 }
 
 size_t ftcnn_report_bytes(int32_t cap_fixes) {

@@ -69,7 +69,9 @@ __global__ __launch_bounds__(kThreads) void coc_kernel(Geom g, const double *__r
             const int ih = g.U * x + r - g.P, iw = g.U * y + s - g.P;
             if (ih < 0 || ih >= g.H || iw < 0 || iw >= g.W) continue;
             const long long ia = ((long long)c * g.H + ih) * g.W + iw;
-            const double x1 = cd1[ia], w1 = cw1[k];
+            const double x1 = cd1[ia];
+            // cw1 is NULL when only Co6 (= Cd1 (x) Cw2) is asked for
+            const double w1 = cw1 ? cw1[k] : 0.0;
             s11 = fma(x1, w1, s11);
             if (cw2) s12 = fma(x1, cw2[k], s12);
             if (cd2) s21 = fma(cd2[ia], w1, s21);
@@ -194,11 +196,12 @@ hipError_t launch_checksum_conv(const Plan &pl, uint32_t which, const void *D, c
         double *o5 = (which & FTCNN_CO5) ? ck.co5 : nullptr;
         double *o6 = (which & FTCNN_CO6) ? ck.co6 : nullptr;
         double *o7 = (which & FTCNN_CO7) ? ck.co7 : nullptr;
+        const double *cw1 = (o5 || o7) ? ck.cw1 : nullptr;
         const double *cw2 = o6 ? ck.cw2 : nullptr;
         const double *cd2 = o7 ? ck.cd2 : nullptr;
 #define COC(TPP)                                                                                    \
     coc_kernel<TPP><<<(unsigned)((g.EF + kThreads / TPP - 1) / (kThreads / TPP)), kThreads, 0, st>>>( \
-        g, ck.cd1, cd2, ck.cw1, cw2, o5, o6, o7)
+        g, ck.cd1, cd2, cw1, cw2, o5, o6, o7)
         if (g.K <= 64) COC(16);
         else if (g.EF <= 4096) COC(256);
         else COC(64);

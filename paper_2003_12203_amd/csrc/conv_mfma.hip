@@ -878,7 +878,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                             f1[j] += v;
                             f6[j] = fmaf(wm, v, f6[j]);
                             fq[j] = fmaf(v, v, fq[j]);
-                            obase[j][mo * g.EF] = b;
+                            obase[j][(long long)mo * g.EF] = b;
                         }
                     }
                 }
@@ -904,7 +904,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                             s1[j] += v;
                             s6[j] = fma(wm, v, s6[j]);
                             sq[j] = fma(v, v, sq[j]);
-                            obase[j][mo * g.EF] = b;
+                            obase[j][(long long)mo * g.EF] = b;
                         }
                     }
                 }
@@ -1040,6 +1040,9 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
 // One tile configuration, dispatched on the weight alignment and the epilogue.
 template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     static constexpr int TM = WM * FM * 32;
+    static constexpr int TP = WP * FP * 32;
+    static constexpr int TK = Tr::TK;
+    static constexpr int WEAVE_KIND = WEAVE;
     static constexpr int NT = Cfg<Tr, WM, WP, FM, FP>::NT;
     static constexpr size_t LDS_BYTES = Cfg<Tr, WM, WP, FM, FP>::LDS_BYTES;
     // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
@@ -1117,8 +1120,21 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
 
 }  // namespace
 
-int conv_tile_m(const Geom &g) {
-    return with_tile(g, nhwc_layer(g), [](auto t) { return decltype(t)::TM; });
+void conv_tile_info(const Geom &g, bool nhwc, int out[6]) {
+    with_tile(g, nhwc, [&](auto t) {
+        using Tt = decltype(t);
+        out[0] = Tt::TM;
+        out[1] = Tt::TP;
+        out[2] = Tt::TK;
+        out[3] = Tt::WEAVE_KIND;
+        out[4] = nhwc ? 1 : 0;
+        out[5] = (nhwc && g.G > 1 && Tt::WEAVE_KIND != 2 && Tt::WEAVE_KIND != 3) ? 1 : 0;
+        return 0;
+    });
+}
+
+int conv_tile_m(const Geom &g, bool nhwc) {
+    return with_tile(g, nhwc, [](auto t) { return decltype(t)::TM; });
 }
 
 hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hipStream_t st, const float *bias) {
@@ -1126,8 +1142,8 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
     return with_tile(pl.g, false, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
-void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes) {
-    with_tile(g, nhwc_layer(g), [&](auto t) {
+void conv_tile_shape(const Geom &g, bool nhwc, int *threads, size_t *lds_bytes) {
+    with_tile(g, nhwc, [&](auto t) {
         *threads = decltype(t)::NT;
         *lds_bytes = decltype(t)::LDS_BYTES;
         return 0;

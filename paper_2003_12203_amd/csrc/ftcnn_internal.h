@@ -181,10 +181,13 @@ hipError_t launch_bias_sums(const Plan &pl, const float *bias, double *c1, doubl
 hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
                             ftcnn_report *rep, int cap, const ftcnn_fault *faults, int nf, void *ws,
                             hipStream_t st, bool cd_given = false);
+// The convolution kernel chosen for this layer (ftcnn_conv_tile): tile rows, pixels, chunk depth,
+// main-loop kind, channels-last, grouped channel skip.
+void conv_tile_info(const Geom &g, bool nhwc, int out[6]);
 // Rows of C per workgroup tile of the convolution chosen for this layer.
-int conv_tile_m(const Geom &g);
+int conv_tile_m(const Geom &g, bool nhwc);
 // Threads per workgroup and dynamic LDS bytes of the convolution chosen for this layer.
-void conv_tile_shape(const Geom &g, int *threads, size_t *lds_bytes);
+void conv_tile_shape(const Geom &g, bool nhwc, int *threads, size_t *lds_bytes);
 // Layers whose convolution reads channels-last copies (pl.nhwc): Ch a multiple of 32 (and
 // kernels of at most 4096 taps, whose weight rows the copy stages in LDS).
 inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0 && g.R * g.S <= 4096; }
