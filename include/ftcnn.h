@@ -326,6 +326,23 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
                          ftcnn_report *rep, int32_t cap_fixes, void *workspace,
                          hipStream_t stream);
 
+/* ftcnn_protected_conv for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the same two or three
+ * launches with no workspace argument.  Scratch comes from a static device array of the
+ * library, 128 MiB on each device, which that device holds from the first call there until
+ * the process ends; nothing is allocated or freed by the call.  The call uses the plan of
+ * ftcnn_protected_conv when that plan's workspace (ftcnn_workspace_bytes) fits the array, and
+ * otherwise the plan without channels-last copies, whose convolution gathers from D as given
+ * (the same results within the output tolerance; K summed in (ch, r, s) order); a layer that
+ * needs more than 128 MiB even then is rejected with FTCNN_E_WORKSPACE before any launch.
+ * The device is the stream's (the current device for the NULL stream).  Every call on one
+ * device shares that device's array and leaves its contents behind; calls whose work overlaps
+ * on one device (other streams, other threads) race on it and must be ordered by the caller.
+ * Arguments, outputs and report as ftcnn_protected_conv. */
+int ftcnn_protected_conv_noalloc(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                                 const ftcnn_checksums *ck, const ftcnn_policy *policy,
+                                 ftcnn_report *rep, int32_t cap_fixes, hipStream_t stream);
+
 /* INSTRUMENTATION (measurement, not an operation of the paper): the next call
  * on the calling thread that launches the convolution kernel (ftcnn_conv_fwd,
  * ftcnn_conv_fwd_ws, ftcnn_conv_fwd_sums, ftcnn_protected_conv) records

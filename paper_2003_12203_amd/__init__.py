@@ -190,6 +190,14 @@ def protected_conv(desc, D, W, O, ck, policy, report, cap, workspace, stream=Non
                                       _stream(stream)), "ftcnn_protected_conv")
 
 
+def protected_conv_noalloc(desc, D, W, O, ck, policy, report, cap, stream=None) -> None:
+    """ftcnn_protected_conv_noalloc: the protected layer with the library's static device scratch in
+    place of a workspace (for callers that cannot allocate)."""
+    _check(lib().ftcnn_protected_conv_noalloc(C.byref(desc), _ptr(D), _ptr(W), _ptr(O), C.byref(ck),
+                                              C.byref(policy), _ptr(report), cap, _stream(stream)),
+           "ftcnn_protected_conv_noalloc")
+
+
 def set_kernel_events(before, after) -> None:
     """ftcnn_set_kernel_events: record two torch.cuda.Event objects (timing enabled) around the next
     launch of the convolution kernel on this thread.  The events are recorded once here first so

@@ -57,7 +57,8 @@ EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ft
            "ftcnn_encode", "ftcnn_conv_fwd", "ftcnn_checksum_conv", "ftcnn_verify", "ftcnn_correct",
            "ftcnn_verify_correct", "ftcnn_conv_fwd_ws", "ftcnn_conv_fwd_sums", "ftcnn_verify_correct_sums", "ftcnn_protected_conv",
            "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias", "ftcnn_check_weights",
-           "ftcnn_relu_pool", "ftcnn_relu_pool_encode", "ftcnn_conv_fwd_sums_given", "ftcnn_conv_tile")
+           "ftcnn_relu_pool", "ftcnn_relu_pool_encode", "ftcnn_conv_fwd_sums_given", "ftcnn_conv_tile",
+           "ftcnn_protected_conv_noalloc")
 
 _lib = None
 
@@ -116,6 +117,9 @@ def load(path: str = LIB_PATH):
     L.ftcnn_protected_conv.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp,
                                        C.c_int32, _dp, _dp]
     L.ftcnn_protected_conv.restype = C.c_int
+    L.ftcnn_protected_conv_noalloc.argtypes = [P(ConvDesc), _dp, _dp, _dp, P(Checksums), P(Policy), _dp,
+                                               C.c_int32, _dp]
+    L.ftcnn_protected_conv_noalloc.restype = C.c_int
     L.ftcnn_inject.argtypes = [P(ConvDesc), _dp, P(Fault), C.c_int32, _dp]
     L.ftcnn_inject.restype = C.c_int
     L.ftcnn_set_kernel_events.argtypes = [_dp, _dp]

@@ -465,6 +465,32 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
                                   stream);
 }
 
+int ftcnn_protected_conv_noalloc(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
+                                 const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
+                                 int32_t cap_fixes, hipStream_t stream) {
+    // the plan of ftcnn_protected_conv when its workspace fits the static scratch, else the plan
+    // without channels-last copies (a smaller workspace, the same results within the output
+    // tolerance: K is summed in (c, r, s) order instead of (r, s, c))
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (pl.bytes > kStaticScratchBytes) {
+        FT_TRY(make_plan(desc, &pl, false));
+        if (pl.bytes > kStaticScratchBytes)
+            return fail(FTCNN_E_WORKSPACE, "protected_conv_noalloc: the layer needs %zu bytes of scratch, the "
+                        "static scratch holds %zu", pl.bytes, kStaticScratchBytes);
+    }
+    FT_TRY(check_policy(policy));
+    if (!ck || !D || !W || !O || !rep) return fail(FTCNN_E_ARG, "protected_conv_noalloc: null pointer");
+    if (!ck->cd1 || !ck->cd2) return fail(FTCNN_E_ARG, "protected_conv_noalloc needs cd1 and cd2");
+    int dev = 0;
+    if (stream) FT_HIP(hipStreamGetDevice(stream, &dev), "protected_conv_noalloc: stream device");
+    else FT_HIP(hipGetDevice(&dev), "protected_conv_noalloc: current device");
+    void *ws = nullptr;
+    FT_HIP(static_scratch(dev, &ws), "protected_conv_noalloc: static scratch");
+    FT_TRY(do_conv_sums(pl, D, W, O, ck, rep, cap_fixes, nullptr, 0, ws, stream));
+    return do_verify_correct_sums(pl, D, W, O, ck, policy, rep, FTCNN_CO5 | FTCNN_CO6 | FTCNN_CO7, ws, stream);
+}
+
 int ftcnn_check_weights(const ftcnn_conv_desc *desc, const void *W, const double *cw1, int32_t *mismatches,
                         void *workspace, hipStream_t stream) {
     Plan pl;

@@ -67,6 +67,8 @@ struct Plan {
 };
 
 constexpr int kThreads = 256;
+// Bytes of the static device scratch that ftcnn_protected_conv_noalloc uses in place of a workspace.
+constexpr size_t kStaticScratchBytes = size_t(128) << 20;
 constexpr int kPrepBatch = 8;   // images per load round of the channels-last copy
 constexpr int kMaxFaults = 64;
 constexpr double kUAcc = 5.9604644775390625e-08;   // 2^-24, fp32 accumulation unit roundoff
@@ -246,5 +248,8 @@ inline int final_tpp(int splits, int taps, long long positions) {
     return t > kThreads ? kThreads : t;
 }
 hipError_t launch_inject(const Plan &pl, void *O, const ftcnn_fault *f, int nf, hipStream_t st);
+// Device address of the static scratch (kStaticScratchBytes, 256-byte aligned) on `device`; looked up
+// once per device with that device current, then cached.
+hipError_t static_scratch(int device, void **ptr);
 
 }  // namespace ftcnn

@@ -161,3 +161,19 @@ def test_chain_links_and_mismatches_on_host():
         network.Chain([(2, 3, 16, 16, 8, 3, 3, 1, 1), (2, 6, 16, 16, 8, 3, 3, 1, 1)], "f32", device="cpu")
     with pytest.raises(ft.FtcnnError):   # 16 -> 7: no 2x2/2 or 3x3/2 pooling fits exactly
         network.Chain([(2, 3, 16, 16, 8, 3, 3, 1, 1), (2, 8, 7, 7, 8, 3, 3, 1, 1)], "f32", device="cpu")
+
+
+def test_noalloc_rejects_layers_beyond_the_static_scratch_without_launch():
+    """ftcnn_protected_conv_noalloc checks the layer's scratch need against its static array (128 MiB)
+    on the host, before any device work: 1024 images x 1024 filters of 64 x 64 outputs need about
+    1 GiB of epilogue partial sums even without channels-last copies."""
+    L = _lib.load()
+    d = ft.make_desc(1024, 32, 64, 64, 1024, 1, 1)
+    ck = _lib.Checksums()
+    pol = ft.make_policy()
+    p = C.c_void_p(256)
+    assert L.ftcnn_protected_conv_noalloc(C.byref(d), p, p, p, C.byref(ck), C.byref(pol), p, 4, None) == -4
+    assert "static scratch" in ft.last_error()
+    # a bad descriptor is still a shape error
+    bad = ft.make_desc(0, 3, 8, 8, 4, 3, 3)
+    assert L.ftcnn_protected_conv_noalloc(C.byref(bad), p, p, p, C.byref(ck), C.byref(pol), p, 4, None) == -2
