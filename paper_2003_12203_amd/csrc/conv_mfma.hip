@@ -294,6 +294,62 @@ __device__ inline typename C::Mask load_b_nhwc(const typename C::T *__restrict__
     return ok ? all : 0u;
 }
 
+// Chunks of K on channels-last operands, each TK consecutive channels of one tap (r, s), walked
+// with the channel blocks outer and the taps inner: the input window of one block of channels is
+// read for all R*S taps of a tile while it is still in the L2 of the tile's XCD (with the taps
+// outer, a tile's window over all channels was evicted before the next tap came back to it).
+// The state is wave-uniform and advances by additions only (scalar registers, no divisions).
+struct TapWalk {
+    int r, s, c0;        // the chunk: tap (r, s), channels [c0, c0 + TK)
+    __device__ inline void next(const Geom &g, int tk) {
+        ++s;
+        if (s == g.S) {
+            s = 0;
+            ++r;
+            if (r == g.R) {
+                r = 0;
+                c0 += tk;
+            }
+        }
+    }
+    __device__ inline int kb(const Geom &g) const { return (r * g.S + s) * g.C + c0; }
+};
+
+// A 16-byte unit in global memory (address space 1): loads through it are global loads that the
+// compiler knows cannot alias the thread's private arrays, which then stay in registers.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 glb_u32x4;
+__device__ inline uint4 load16(uintptr_t a) {
+    return __builtin_bit_cast(uint4, *reinterpret_cast<const glb_u32x4 *>(a));
+}
+
+// The gathers of one chunk for the TapWalk loops, as raw 16-byte loads: a slot outside the
+// operands (a weight row past M, a tap in the zero padding) loads from the 256-byte zero page
+// instead, so no select waits on the loaded data and the loads stay in flight across the MFMAs
+// of the current chunk.  Addresses are selected as integers (a pointer select becomes a branch).
+template <typename C>
+__device__ inline void load_a_tap(const typename C::T *__restrict__ Wt, int kb, const ASlots<C> &as, uintptr_t zpa,
+                                  Pack<typename C::T, C::VEC> (&ra)[C::A_PER]) {
+#pragma unroll
+    for (int i = 0; i < C::A_PER; ++i) {
+        const uintptr_t src = as.base[i] >= 0 ? reinterpret_cast<uintptr_t>(Wt + as.base[i] + kb) : zpa;
+        ra[i].q = load16(src);
+    }
+}
+
+// The B gather: the thread's KR channels of its pixel's input at tap (r, s).  pix_off = image
+// base + (ih0 W + iw0) C + the thread's channel offset in the chunk.
+template <typename C>
+__device__ inline void load_b_tap(const typename C::T *__restrict__ Dt, const Geom &g, const TapWalk &t, bool pvalid,
+                                  int pix_off, int ih0, int iw0, uintptr_t zpa,
+                                  Pack<typename C::T, C::VEC> (&rb)[C::KR / C::VEC]) {
+    const bool ok = pvalid & ((unsigned)(ih0 + t.r) < (unsigned)g.H) & ((unsigned)(iw0 + t.s) < (unsigned)g.W);
+    const int off = pix_off + (t.r * g.W + t.s) * g.C + t.c0;
+    const uintptr_t src = ok ? reinterpret_cast<uintptr_t>(Dt + off) : zpa;
+#pragma unroll
+    for (int i = 0; i < C::KR / C::VEC; ++i) rb[i].q = load16(src + 16 * i);
+}
+
 // Stateful form of the B gather, so that its elements can be issued one at a
 // time between MFMAs: (c, r, s) and the k offset advance in scalar registers.
 template <typename C> struct BGather {
@@ -653,10 +709,26 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         return j * C::TK;
     };
     typename C::Mask amask = 0, bmask = 0;
+    // channels-last loops other than the two-in-flight one: chunks walked by TapWalk, channel
+    // blocks [cg0, cg0 + TK * (nch / (R S))) outer, taps inner
+    constexpr bool TAPS = NHWC && !DMA && WEAVE != 2;
+    TapWalk tw{0, 0, 0};
+    int pix_off = 0;
+    const uintptr_t zpa = reinterpret_cast<uintptr_t>(zp);   // 256 zero bytes (channels-last layers)
+    if constexpr (TAPS) {
+        tw.c0 = cg0;
+        if (!(KSKIP && cpr > 0)) nch = g.R * g.S * (g.C / C::TK);
+        pix_off = lane_base + (ih0 * g.W + iw0) * g.C + bkg * C::KR;
+    }
     if constexpr (!DMA) {
-        amask = load_a<C>(Wt, g, kbase(0), KVEC, as, ra);
-        bmask = NHWC ? load_b_nhwc<C>(D, g, kbase(0) + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
-                     : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+        if constexpr (TAPS) {
+            load_a_tap<C>(Wt, tw.kb(g), as, zpa, ra);
+            load_b_tap<C>(D, g, tw, pvalid, pix_off, ih0, iw0, zpa, rb);
+        } else {
+            amask = load_a<C>(Wt, g, kbase(0), KVEC, as, ra);
+            bmask = NHWC ? load_b_nhwc<C>(D, g, kbase(0) + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb)
+                         : load_b<C>(D, g, bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+        }
         store_lds<C, NHWC>(As0, Bs0, tid, ra, amask, rb, bmask, bp, bkg);
         __syncthreads();
     }
@@ -693,13 +765,17 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         if (kc < nchunks) mma_chunk<C, FM, FP>(A0, B0, lane, arow0, brow0, acc);   // odd count: the last chunk
     } else if constexpr (NHWC) {
         // channels-last: a whole chunk's gather is a few 16-byte loads per thread, issued
-        // before this chunk's MFMAs and stored after them
+        // before this chunk's MFMAs and stored after them.  The scheduling fences keep the
+        // compiler from sinking the loads next to their stores: they then have the whole
+        // chunk of MFMAs to land instead of a few.
         for (int kc = 0; kc + 1 < nch; ++kc) {
             const int buf = kc & 1;
-            const int kb = kbase(kc + 1);
-            amask = load_a<C>(Wt, g, kb, KVEC, as, ra);
-            bmask = load_b_nhwc<C>(D, g, kb + bkg * C::KR, pvalid, lane_base, ih0, iw0, rb);
+            tw.next(g, C::TK);
+            load_a_tap<C>(Wt, tw.kb(g), as, zpa, ra);
+            load_b_tap<C>(D, g, tw, pvalid, pix_off, ih0, iw0, zpa, rb);
+            __builtin_amdgcn_sched_barrier(0);
             mma_chunk<C, FM, FP>(As0 + buf * C::TM * C::LDK, Bs0 + buf * C::TP * C::LDK, lane, arow0, brow0, acc);
+            __builtin_amdgcn_sched_barrier(0);
             store_lds<C, NHWC>(As0 + (buf ^ 1) * C::TM * C::LDK, Bs0 + (buf ^ 1) * C::TP * C::LDK, tid, ra, amask, rb,
                          bmask, bp, bkg);
             __syncthreads();
