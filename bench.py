@@ -170,7 +170,8 @@ def kernel_key(ft, lay, path=1):
 
 def kernel_label(key, dtype):
     tm, tp, tk, loop, nhwc, skip = key
-    kinds = {0: "register-staged", 1: "gather woven between MFMAs", 2: "two chunks in flight", 3: "direct-to-LDS"}
+    kinds = {0: "register-staged", 1: "gather woven between MFMAs", 2: "two chunks in flight", 3: "direct-to-LDS",
+             4: "direct-to-LDS, three stages"}
     return (f"conv_kernel {dtype} {tm}x{tp} tile, {tk}-deep chunks, {kinds[loop]}"
             f"{', channels-last' if nhwc else ', NCHW gather'}{', grouped channel skip' if skip else ''}")
 
@@ -213,6 +214,14 @@ def main():
 
     ft.lib()  # fails loudly if the HIP library is missing
     torch.cuda.set_device(0)
+    if args.copy_calibration_mib > 0:
+        # a plain copy of known size: the scale of FETCH_SIZE / WRITE_SIZE per byte moved
+        a = torch.ones(args.copy_calibration_mib << 18, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(2):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     cfg = workload_config(args.workload)
     if args.groups and args.workload != "alexnet":
         print("bench.py: --groups applies to the AlexNet workload (Caffe's two groups)", file=sys.stderr)
@@ -230,14 +239,6 @@ def main():
     nl = len(runs)
     total_flops = sum(r.flops for r in runs)
     torch.cuda.synchronize()
-    if args.copy_calibration_mib > 0:
-        # a plain copy of known size: the scale of FETCH_SIZE / WRITE_SIZE per byte moved
-        a = torch.ones(args.copy_calibration_mib << 18, device="cuda")
-        b = torch.empty_like(a)
-        for _ in range(2):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
 
     # the dominant kernel for the roofline: the convolution instantiation that carries the most
     # flops of the step (on VGG-19 fp32 the 128 x 128 channels-last tile of v3-v12); every one of
@@ -854,6 +855,34 @@ def summarize_profile(args):
                 continue
             emit(f"| `{nm}` | {grid} | {a['n']} | " + " | ".join(f"{v:.6g}" for v in vals) + " |")
         emit("")
+        # achieved HBM bandwidth of the memory-bound kernels: calibrated FETCH + WRITE bytes of a
+        # dispatch over its duration in the kernel trace of the same command (matched by name and grid)
+        if trace and scale_f and scale_w:
+            tdur = {}
+            for r in trace:
+                k = (_short(r["Kernel_Name"]), int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"]))
+                tdur.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+            emit("Memory-bound kernels (FETCH + WRITE per dispatch, calibrated; duration from the kernel trace):")
+            emit("")
+            emit("| kernel | grid (threads) | dispatches | MB read | MB written | avg us | GB/s | of 8 TB/s |")
+            emit("|---|---:|---:|---:|---:|---:|---:|---:|")
+            rows_bw = []
+            for (nm, grid), a in agg.items():
+                if nm.startswith("conv_kernel") or "copyBuffer" in nm or "FETCH_SIZE" not in a or "WRITE_SIZE" not in a:
+                    continue
+                if (nm, grid) not in tdur:
+                    continue
+                rb = a["FETCH_SIZE"] / a["n"] * 1024 * scale_f
+                wb = a["WRITE_SIZE"] / a["n"] * 1024 * scale_w
+                us = sum(tdur[(nm, grid)]) / len(tdur[(nm, grid)]) / 1e3
+                if rb + wb < 1e6:
+                    continue
+                rows_bw.append((nm, grid, a["n"], rb, wb, us))
+            for nm, grid, n, rb, wb, us in sorted(rows_bw, key=lambda x: -(x[3] + x[4])):
+                gbs = (rb + wb) / us / 1e3
+                emit(f"| `{nm}` | {grid} | {n} | {rb / 1e6:.1f} | {wb / 1e6:.1f} | {us:.1f} | {gbs:.0f} | "
+                     f"{gbs / 1e3 / HBM_PEAK_TBS:.2f} |")
+            emit("")
         # the dominant kernel's traffic and matrix-core busy fraction, per launch
         fsum = wsum = busy = gui = mops = 0.0
         nd = 0

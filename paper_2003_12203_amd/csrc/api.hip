@@ -147,12 +147,14 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
         co.ns = pl->prep_ns;
         co.comb_blocks = pl->prep_ns > 1 ? (int)ceil_div(CHW, 2LL * nt) : 0;
     }
+    // 256 zero bytes for loads that fall outside the operands (written by the copy), directly in
+    // front of Dt: the direct-to-LDS loads reach both through one buffer descriptor
+    pl->off_zero = off;
+    off += pl->nhwc ? 256 : 0;
     pl->off_dt = off;
     off += pl->nhwc ? align256((size_t)g.N * CHW * es) : 0;
     pl->off_wt = off;
     off += pl->nhwc ? align256((size_t)g.M * K * es) : 0;
-    pl->off_zero = off;   // 256 zero bytes for loads that fall outside the operands (written by the copy)
-    off += pl->nhwc ? 256 : 0;
     pl->off_encp = off;
     off += pl->prep_ns > 1 ? align256(2ull * pl->prep_ns * CHW * sizeof(double)) : 0;
     pl->off_copart = off;

@@ -56,7 +56,8 @@ template <int TK_> struct BF16T {
     static constexpr int VEC = 8;
 };
 
-template <typename Tr, int WM, int WP, int FM, int FP, bool KVEC_ = true>
+// DSTAGES > 0: the direct-to-LDS loop with that many stages of (TM + TP) rows of 128 bytes.
+template <typename Tr, int WM, int WP, int FM, int FP, bool KVEC_ = true, int DSTAGES = 0>
 struct Cfg {
     using T = typename Tr::T;
     static constexpr bool KVEC = KVEC_;   // W rows 16-byte aligned: whole-slot weight loads
@@ -74,7 +75,8 @@ struct Cfg {
     static_assert(KR <= 64 && A_PER * VEC <= 64, "gather masks are at most 64-bit");
     // one bit per gathered element of a thread
     using Mask = typename std::conditional<(KR > 32 || A_PER * VEC > 32), uint64_t, uint32_t>::type;
-    static constexpr size_t LDS_BYTES = 2ull * (TM + TP) * LDK * sizeof(T);
+    static constexpr size_t LDS_BYTES = DSTAGES > 0 ? (size_t)DSTAGES * (TM + TP) * 128
+                                                    : 2ull * (TM + TP) * LDK * sizeof(T);
     static_assert(LDS_BYTES <= 160 * 1024, "tile exceeds the LDS of a CU");
 };
 
@@ -493,74 +495,115 @@ __device__ inline void mma_chunk_swz(const unsigned char *As, const unsigned cha
     }
 }
 
-// The whole K loop of one tile.  zp: 16 zero bytes that lanes whose row or tap
-// lies outside the operands load instead.  Needs Ch % 64 == 0 (a chunk is one
-// (r, s) tap of 64 channels) and 2 * (TM + TP) * 128 bytes of LDS.
-template <typename C, int FM, int FP>
-__device__ inline void dma_mainloop(const uint16_t *__restrict__ Dt, const uint16_t *__restrict__ Wt, const Geom &g,
-                                    int m0, long long p0, const uint16_t *zp, unsigned char *smem,
-                                    floatx16 (&acc)[FM][FP], int tid, int arow0, int brow0) {
+// A raw buffer descriptor over [base, base + bytes) (stride 0, the data-format word of gfx9
+// buffer resources), and a 16-byte load through it straight into LDS: lane L writes lds + 16 L.
+__device__ inline __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, 0x00020000);
+}
+__device__ inline void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, unsigned char *lds, unsigned voff, unsigned soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t *)lds, 16, voff, soff, 0, 0);
+}
+
+// s_waitcnt vmcnt for a count known only at run time (the chunks still in flight behind the one
+// about to be consumed): at most STAGES - 1 chunks of NI loads each.
+template <int NI, int STAGES> __device__ inline void wait_chunks_behind(int behind) {
+    if constexpr (STAGES > 2) {
+        if (behind >= 2) {
+            wait_vmcnt<2 * NI>();
+            return;
+        }
+    }
+    if (behind >= 1) wait_vmcnt<NI>();
+    else wait_vmcnt<0>();
+}
+
+// The whole K loop of one tile, with buffer loads straight into LDS (buffer_load_dwordx4 ... lds:
+// lane L of a wave lands at the LDS base + 16 L, the base wave-uniform).  Two buffer descriptors:
+// the weights Wt, and the zero page followed by Dt (256 zero bytes in front of the channels-last
+// input in the workspace).  A weight slot's offset is fixed for the tile (rows past M read row
+// M - 1: their outputs are never stored) and the chunk's k goes into the scalar offset; an input
+// slot's offset is its pixel's base plus the chunk's tap offset, or 0 (the zero page) for a tap in
+// the padding.  So a chunk costs a few vector instructions per input slot and none per weight
+// slot.  Chunks follow TapWalk (channel blocks of 64 outer, taps inner) through a ring of STAGES
+// LDS stages: chunk k + STAGES - 1 is requested as soon as every wave has read chunk k - 1's
+// stage, so a chunk's loads have STAGES - 1 chunks of MFMAs to land.  Needs Ch % 64 == 0.
+template <typename C, int FM, int FP, int STAGES>
+__device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom &g, int m0, long long p0,
+                                    const unsigned char *zp_dt, unsigned char *smem, floatx16 (&acc)[FM][FP],
+                                    int tid, int arow0, int brow0) {
     constexpr int NW = C::NT / 64;
     constexpr int NIA = C::TM / (8 * NW), NIB = C::TP / (8 * NW), NI = NIA + NIB;
-    static_assert(C::TM % (8 * NW) == 0 && C::TP % (8 * NW) == 0 && NI < 64, "DMA tile shape");
+    static_assert(C::TM % (8 * NW) == 0 && C::TP % (8 * NW) == 0 && (STAGES - 1) * NI < 64, "DMA tile shape");
     constexpr int STAGE_A = C::TM * 128, STAGE = (C::TM + C::TP) * 128;
     const int lane = tid & 63, w = tid >> 6;
     const int lr = lane >> 3;              // row of the instruction's eight
     const int cg = (lane & 7) ^ lr;        // global chunk this lane loads (its LDS chunk is lane & 7)
-    int a_off[NIA];
-    bool a_ok[NIA];
+    const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(Wt, (int)((long long)g.M * g.K * 2));
+    const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(zp_dt, (int)(256 + (long long)g.N * g.CHW * 2));
+    unsigned a_off[NIA];
 #pragma unroll
     for (int j = 0; j < NIA; ++j) {
-        const int m = m0 + (j * NW + w) * 8 + lr;
-        a_ok[j] = m < g.M;
-        a_off[j] = (a_ok[j] ? m : 0) * g.K + cg * 8;
+        int m = m0 + (j * NW + w) * 8 + lr;
+        m = m < g.M ? m : g.M - 1;
+        a_off[j] = (unsigned)(m * g.K + cg * 8) * 2u;
     }
-    int b_base[NIB], b_ih[NIB], b_iw[NIB];
-    bool b_ok[NIB];
+    unsigned b_off[NIB];
+    int b_ih[NIB], b_iw[NIB];
 #pragma unroll
     for (int j = 0; j < NIB; ++j) {
-        const long long pg = p0 + (j * NW + w) * 8 + lr;
-        b_ok[j] = pg < g.P_total;
-        const int n = b_ok[j] ? (int)(pg / g.EF) : 0;
-        const int pix = b_ok[j] ? (int)(pg - (long long)n * g.EF) : 0;
+        long long pg = p0 + (j * NW + w) * 8 + lr;
+        pg = pg < g.P_total ? pg : g.P_total - 1;   // columns past the end are never stored
+        const int n = (int)(pg / g.EF);
+        const int pix = (int)(pg - (long long)n * g.EF);
         const int x = pix / g.F, y = pix - (pix / g.F) * g.F;
         b_ih[j] = g.U * x - g.P;
         b_iw[j] = g.U * y - g.P;
-        b_base[j] = n * (int)g.CHW + cg * 8;
+        // 32-bit wrap-around arithmetic: the sum with a valid tap's offset is the element's offset
+        b_off[j] = 256u + 2u * (unsigned)(n * (int)g.CHW + (b_ih[j] * g.W + b_iw[j]) * g.C + cg * 8);
     }
-    const uintptr_t zpa = reinterpret_cast<uintptr_t>(zp);
-    auto issue = [&](int kc, int st) {
-        const int kb = kc * 64;
-        const int rs = kb / g.C, c0 = kb - rs * g.C;
-        const int r = rs / g.S, s = rs - (rs / g.S) * g.S;
-        unsigned char *base = smem + st * STAGE;
+    // part q (of 4) of a chunk's loads: a quarter of the weight and of the input slots
+    static_assert(NIA % 4 == 0 && NIB % 4 == 0, "DMA slots split over the four k-steps");
+    auto issue_part = [&](const TapWalk &t, unsigned char *base, int q) {
+        const unsigned soff_a = 2u * (unsigned)t.kb(g);
+        const unsigned tap = 2u * (unsigned)((t.r * g.W + t.s) * g.C + t.c0);
 #pragma unroll
-        for (int j = 0; j < NIA; ++j) {
-            // the address is selected as an integer: a pointer select would become a branch
-            const uintptr_t src = a_ok[j] ? reinterpret_cast<uintptr_t>(Wt + a_off[j] + kb) : zpa;
-            __builtin_amdgcn_global_load_lds((glb_cvoid_t *)src, (lds_void_t *)(base + (j * NW + w) * 8 * 128), 16, 0, 0);
+        for (int jj = 0; jj < NIA / 4; ++jj) {
+            const int j = q * (NIA / 4) + jj;
+            buffer_load_lds16(rw, base + (j * NW + w) * 8 * 128, a_off[j], soff_a);
         }
 #pragma unroll
-        for (int j = 0; j < NIB; ++j) {
-            const int ih = b_ih[j] + r, iw = b_iw[j] + s;
-            const bool ok = b_ok[j] & ((unsigned)ih < (unsigned)g.H) & ((unsigned)iw < (unsigned)g.W);
-            const uintptr_t src = ok ? reinterpret_cast<uintptr_t>(Dt + b_base[j] + (ih * g.W + iw) * g.C + c0) : zpa;
-            __builtin_amdgcn_global_load_lds((glb_cvoid_t *)src,
-                                             (lds_void_t *)(base + STAGE_A + (j * NW + w) * 8 * 128), 16, 0, 0);
+        for (int jj = 0; jj < NIB / 4; ++jj) {
+            const int j = q * (NIB / 4) + jj;
+            const bool ok = ((unsigned)(b_ih[j] + t.r) < (unsigned)g.H) & ((unsigned)(b_iw[j] + t.s) < (unsigned)g.W);
+            buffer_load_lds16(rd, base + STAGE_A + (j * NW + w) * 8 * 128, ok ? b_off[j] + tap : 0u, 0u);
         }
     };
-    const int nch = g.K / 64;
-    issue(0, 0);
-    if (nch > 1) issue(1, 1);
+    const int nch = g.R * g.S * (g.C / 64);
+    TapWalk ti{0, 0, 0};
+#pragma unroll
+    for (int st = 0; st + 1 < STAGES; ++st) {
+        if (st < nch) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) issue_part(ti, smem + st * STAGE, q);
+            ti.next(g, 64);
+        }
+    }
     for (int kc = 0; kc < nch; ++kc) {
-        if (kc + 1 < nch) wait_vmcnt<NI>();   // this wave's loads of chunk kc have landed
-        else wait_vmcnt<0>();
-        lds_barrier();                        // ... and every wave's
-        const unsigned char *st = smem + (kc & 1) * STAGE;
+        // this wave's loads of chunk kc have landed when at most the later chunks' are in flight
+        const int behind = nch - 1 - kc < STAGES - 2 ? nch - 1 - kc : STAGES - 2;
+        wait_chunks_behind<NI, STAGES>(behind);
+        lds_barrier();                        // ... and every wave's; every wave is done with chunk kc - 1
+        // chunk kc + STAGES - 1 goes into the stage chunk kc - 1 used, all of it before this
+        // chunk's MFMAs (spreading the requests between the k-steps measured slower)
+        if (kc + STAGES - 1 < nch) {
+            unsigned char *nbase = smem + ((kc + STAGES - 1) % STAGES) * STAGE;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) issue_part(ti, nbase, q);
+            ti.next(g, 64);
+        }
+        const unsigned char *st = smem + (kc % STAGES) * STAGE;
         mma_chunk_swz<C, FM, FP>(st, st + STAGE_A, lane, arow0, brow0, acc);
         wait_lgkm0();
-        lds_barrier();                        // every wave has read the stage
-        if (kc + 2 < nch) issue(kc + 2, kc & 1);
     }
 }
 
@@ -614,7 +657,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                                                             typename Tr::T *__restrict__ O, Geom g,
                                                             int tiles_m, int tiles_total, int m_major,
                                                             const void *zp, Epi<EPI> ep) {
-    using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
+    using C = Cfg<Tr, WM, WP, FM, FP, KVEC, (WEAVE >= 3 ? WEAVE - 1 : 0)>;
     using T = typename C::T;
     extern __shared__ __align__(16) unsigned char smem[];
     T *As0 = reinterpret_cast<T *>(smem);
@@ -684,7 +727,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    constexpr bool DMA = NHWC && WEAVE == 3 && sizeof(T) == 2 && C::TK == 64;
+    constexpr bool DMA = NHWC && WEAVE >= 3 && sizeof(T) == 2 && C::TK == 64;
     Pack<T, C::VEC> ra[C::A_PER];
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
@@ -734,8 +777,9 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     }
 
     if constexpr (DMA) {
-        dma_mainloop<C, FM, FP>(reinterpret_cast<const uint16_t *>(D), reinterpret_cast<const uint16_t *>(Wt), g, m0,
-                                p0, static_cast<const uint16_t *>(zp), smem, acc, tid, arow0, brow0);
+        // D is the channels-last copy, which the workspace keeps right behind the zero page zp
+        dma_mainloop<C, FM, FP, WEAVE - 1>(reinterpret_cast<const uint16_t *>(Wt), g, m0, p0,
+                                           static_cast<const unsigned char *>(zp), smem, acc, tid, arow0, brow0);
     } else if constexpr (NHWC && WEAVE == 2) {
         // channels-last, two chunks in flight: chunk kc + 2 is loaded into one register set
         // while chunk kc is consumed from LDS, and chunk kc + 1 (loaded a whole chunk earlier,
@@ -1060,7 +1104,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
 template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC, bool GRP = false>
 hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
                       const void *zp, const Epi<EPI> &ep) {
-    using C = Cfg<Tr, WM, WP, FM, FP, KVEC>;
+    using C = Cfg<Tr, WM, WP, FM, FP, KVEC, (WEAVE >= 3 ? WEAVE - 1 : 0)>;
     using T = typename C::T;
     static_assert(EPI == 0 || (size_t)WM * 3 * C::TP * sizeof(double) <= C::LDS_BYTES, "epilogue fold fits LDS");
     const int tiles_m = (g.M + C::TM - 1) / C::TM;
@@ -1120,14 +1164,16 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     static constexpr int TK = Tr::TK;
     static constexpr int WEAVE_KIND = WEAVE;
     static constexpr int NT = Cfg<Tr, WM, WP, FM, FP>::NT;
-    static constexpr size_t LDS_BYTES = Cfg<Tr, WM, WP, FM, FP>::LDS_BYTES;
+    static constexpr size_t LDS_BYTES = Cfg<Tr, WM, WP, FM, FP, true, (WEAVE >= 3 ? WEAVE - 1 : 0)>::LDS_BYTES;
     // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
     template <int EPI>
     static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep,
                           bool nhwc = false, const void *zp = nullptr) {
-        if constexpr (WEAVE == 3) {
-            // direct-to-LDS tiles exist for channels-last operands only
-            if (!nhwc || !zp) return hipErrorInvalidValue;
+        if constexpr (WEAVE >= 3) {
+            // direct-to-LDS tiles exist for channels-last operands only, with the copy of D right
+            // behind the zero page (one buffer descriptor reaches both)
+            if (!nhwc || !zp || static_cast<const char *>(zp) + 256 != static_cast<const char *>(D))
+                return hipErrorInvalidValue;
             return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
         } else {
             if constexpr (WEAVE != 2) {
@@ -1185,8 +1231,11 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
     }
     if (g.M <= 32) return f(BF16_M32{});
     if (g.M <= 64) return f(BF16_M64{});
-    if (nhwc && g.C % 64 == 0) {
-        // direct-to-LDS loads: 256 x 256 where M is large and there are enough such tiles
+    // direct-to-LDS loads reach the operands through 32-bit buffer offsets
+    const bool dma = nhwc && g.C % 64 == 0 && (long long)g.M * g.K * 2 < (1LL << 31) &&
+                     256 + (long long)g.N * g.CHW * 2 < (1LL << 31);
+    if (dma) {
+        // 256 x 256 where M is large and there are enough such tiles
         if (g.M >= 512 && n_tiles(g, 256, 256) >= 192) return f(BF16_DMA_256x256{});
         return f(BF16_DMA_128x128{});
     }
