@@ -239,23 +239,28 @@ int ftcnn_verify(const ftcnn_conv_desc *desc, const void *O, const ftcnn_checksu
                  const ftcnn_policy *policy, ftcnn_report *rep, int32_t cap_fixes,
                  void *workspace, hipStream_t stream);
 
-/* Correction module (Sec. 4.3): one device-gated launch that does nothing
+/* Correction module (Sec. 4.3): two device-gated launches that do nothing
  * unless rep->detected.  Every flagged position runs CoC, then RC and ClC if
  * enabled, then FC (with the fallbacks of Sec. 4.1.5), each scheme undone
  * unless Co5..Co7 agree with the re-summed output afterwards.  Repairs O in
  * place.  Positions where a weighted checksum agrees while Co5 does not are
- * re-checked against checksums re-encoded from D and W (Sec. 4.1.4).  Reads
- * D, W, ck->cd1/cd2/cw1/cw2/co5/co6/co7 and the verify flag map in the
- * workspace.  Leaves status NEEDS_RECOMPUTE if any position is unresolved;
- * the caller then reruns ftcnn_conv_fwd and ftcnn_verify (Sec. 4.1.1). */
+ * re-checked against checksums re-encoded from D and W (Sec. 4.1.4).  The first
+ * launch hands the flagged positions over; the second computes the row and
+ * column checksums Co1..Co4 and the per-filter and per-image summations at
+ * them over the whole device, and its last workgroup takes every decision.
+ * Reads D, W, ck->cd1/cd2/cw1/cw2/co5/co6/co7, ck->so5/so6/so7/q5 when set (as
+ * ftcnn_verify leaves them) and the verify flag map in the workspace.  Leaves
+ * status NEEDS_RECOMPUTE if any position is unresolved; the caller then reruns
+ * ftcnn_conv_fwd and ftcnn_verify (Sec. 4.1.1). */
 int ftcnn_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                   const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                   void *workspace, hipStream_t stream);
 
 /* ftcnn_verify and ftcnn_correct in two launches: the final detection stage
- * runs the correction chain of ftcnn_correct in the same workgroup for every
- * position it flags, so a clean layer pays nothing for the correction module.
- * Same inputs, outputs and report as the two calls in sequence. */
+ * hands every position it flags to the correction's second launch, which does
+ * nothing when none was flagged, so a clean layer pays one empty launch for the
+ * correction module.  Same inputs, outputs and report as the two calls in
+ * sequence. */
 int ftcnn_verify_correct(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                          const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                          int32_t cap_fixes, void *workspace, hipStream_t stream);

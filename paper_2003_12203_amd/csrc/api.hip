@@ -92,10 +92,10 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
     pl->nhwc = allow_nhwc && nhwc_layer(g);
     // summations fused into the convolution epilogue: one slice per (filter tile, image)
     pl->sum_splits = (int)(ceil_div(g.M, conv_tile_m(g, pl->nhwc)) * g.N);
-    // correction: the standalone launch has corr_blocks workgroups, one scratch slice each; in
-    // the fused final stage a workgroup with flagged positions takes the next free slice
+    // correction: the standalone launch hands the flagged positions over from at most corr_blocks
+    // workgroups; every path leaves the chain to the wide stage, whose scratch is laid out by
+    // corr_layout
     pl->corr_blocks = 256;
-    pl->corr_slots = 256;
     const long long L = g.M > g.N ? g.M : g.N;
     pl->corr_stride = (size_t)((4LL * g.M + 4LL * g.N + 2 * L + 31) / 32 * 32);
 
@@ -160,7 +160,7 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
     pl->off_copart = off;
     off += pl->co_in_conv ? align256(3ull * pl->co.groups * pl->prep_ns * EF * sizeof(double)) : 0;
     pl->off_corr = off;
-    off += align256((size_t)pl->corr_slots * pl->corr_stride * sizeof(double));
+    off += align256(corr_layout(g, pl->corr_stride).bytes);
     pl->off_wchk = off;   // Cw1, Cw2 re-encoded by ftcnn_check_weights
     off += align256(2 * sizeof(double) * (size_t)K);
     pl->off_wfull = off;  // grouped layers: the block-diagonal expansion of W

@@ -54,8 +54,7 @@ struct Plan {
     int enc_splits_d, enc_splits_w;   // row splits of the input-checksum reductions
     int ver_splits;                   // row splits of the verification reduction
     int ver_cols_per_block;           // columns handled by one verify block
-    int corr_blocks;                  // workgroups of the correction kernel
-    int corr_slots;                   // per-workgroup scratch slices (correction or fused verification)
+    int corr_blocks;                  // workgroups of the standalone correction kernel
     int sum_splits;                   // partial-sum slices written by the convolution epilogue
     bool nhwc;                        // the convolution reads channels-last copies of D and W
     int prep_ns;                      // image ranges of the encode fused into the channels-last copy
@@ -63,10 +62,58 @@ struct Plan {
     CocTile co;                       // their tiling (co_in_conv)
     size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, off_zero,
         off_wchk, off_wfull, bytes;
-    size_t corr_stride;               // doubles of scratch per correction workgroup
+    size_t corr_stride;               // doubles of the decision stage's per-position arrays
 };
 
 constexpr int kThreads = 256;
+
+// The correction's wide stage (the Sec. 4.3 chain): flagged positions are handed over as Pending
+// records (room for every position of the layer).  The stage's workgroups spread the row and
+// column checksums Co1..Co4 and the per-filter and per-image summations of the first kMaxPending
+// of them (and, for possibly suspect checksums, Co5..Co7 re-encoded from D and W over
+// kFreshRanges ranges of taps) over the whole launch, and the last of them takes those positions'
+// decisions; any further position is taken whole by one workgroup.
+constexpr int kMaxPending = 64;
+constexpr int kFreshRanges = 256;
+constexpr int kRowSums = 6;   // per filter: Co1, Co3 (without bias), So1, So3, sum o^2, sum ((n + wbase) o)^2
+constexpr int kColSums = 5;   // per image: Co2, Co4 (without bias), So2, So4, sum o^2
+struct Pending {
+    int p, mode;     // position; mode 1: a weighted checksum may agree (re-encode Co5..Co7)
+    double co[3];    // Co5..Co7 at p as the summations see them (bias shares added)
+};
+// Workgroups of the wide stage: one per work unit of a position (four filters, or one image), at
+// least kFreshRanges, at most 1024.
+inline int wide_grid(const Geom &g) {
+    const long long need = ((long long)g.M + 3) / 4 + g.N;
+    return (int)(need < kFreshRanges ? kFreshRanges : (need > 1024 ? 1024 : need));
+}
+// Largest window of Cd1 and Cd2 at one position (2 K doubles and K flags) that the wide stage
+// stages in shared memory, so that two of its workgroups still share a compute unit.
+constexpr size_t kWindowBytes = 79 << 10;
+// The wide stage's completion count: kDoneGroups counters (workgroup b counts in b % kDoneGroups),
+// the last arrival of each then in one more, so that no single counter takes every arrival.
+// Counters sit kDoneStride ints (4 KiB) apart, the top one first.
+constexpr int kDoneGroups = 32;
+constexpr int kDoneStride = 1024;
+// Byte offsets inside the correction scratch (the workspace at Plan::off_corr).
+struct CorrLayout {
+    size_t done, pend, rows, cols, fresh, chain, bytes;
+};
+inline CorrLayout corr_layout(const Geom &g, size_t chain_doubles) {
+    auto a256 = [](size_t b) { return (b + 255) & ~size_t(255); };
+    const size_t blocks = (size_t)wide_grid(g);
+    const size_t slabs = (size_t)kMaxPending + blocks;   // the shared batch, then one per workgroup
+    CorrLayout L{};
+    size_t off = 0;
+    L.done = off;  off += a256(sizeof(int) * kDoneStride * (kDoneGroups + 1));
+    L.pend = off;  off += a256(sizeof(Pending) * (size_t)g.EF);
+    L.rows = off;  off += a256(sizeof(double) * kRowSums * (size_t)g.M * slabs);
+    L.cols = off;  off += a256(sizeof(double) * kColSums * (size_t)g.N * slabs);
+    L.fresh = off; off += a256(sizeof(double) * 3 * (size_t)kFreshRanges * kMaxPending);
+    L.chain = off; off += a256(sizeof(double) * chain_doubles * blocks);
+    L.bytes = off;
+    return L;
+}
 // Bytes of the static device scratch that ftcnn_protected_conv_noalloc uses in place of a workspace.
 constexpr size_t kStaticScratchBytes = size_t(128) << 20;
 constexpr int kPrepBatch = 8;   // images per load round of the channels-last copy
