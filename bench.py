@@ -73,6 +73,11 @@ def parse():
                          "recomputation) on each distinct layer, and the layerwise RC/ClC choice (one JSON "
                          "line per layer)")
     ap.add_argument("--scheme-reps", type=int, default=10)
+    ap.add_argument("--fault-protocol", action="store_true",
+                    help="instead of the benchmark: the erroneous-run protocol of Sec. 6.1-6.2, one epoch per "
+                         "layer with a row or column fault pattern in that layer, with RC/ClC disabled and with "
+                         "the layerwise RC/ClC choice (one JSON line)")
+    ap.add_argument("--protocol-rounds", type=int, default=5)
     ap.add_argument("--groups", action="store_true",
                     help="AlexNet with Caffe's two groups on conv2, conv4 and conv5 (Sec. 5.2); flops counted "
                          "for the grouped layers")
@@ -161,6 +166,125 @@ def scheme_table(args, cfg, runs, ft, torch):
         print(json.dumps(line), flush=True)
 
 
+def fault_protocol(args, cfg, runs, ft, torch):
+    """The erroneous-case protocol of Sec. 6.1-6.2: L epochs for L layers, epoch i planting one
+    fault pattern in layer i, every layer protected.  A pattern is a corrupted row (three filters of
+    one image) or column (three images of one filter) of O at the centre position (schemes.pattern),
+    row with probability |D| / (|D| + |W|) (a fault in D corrupts a row, one in W a column, Sec. 4.1),
+    from a seeded draw per layer.  Two policies: RC and ClC disabled on every layer (CoC, then FC),
+    and the layerwise choice of Sec. 4.3 from each layer's measured workflow times.  Each epoch's
+    step is timed in rounds of turns with the error-free protected step and the unprotected one;
+    the overhead is the mean over the epochs of the median step against the unprotected median."""
+    import statistics
+
+    import numpy as np
+
+    from paper_2003_12203_amd import schemes
+
+    nl = len(runs)
+    kinds, patterns = [], []
+    for li, r in enumerate(runs):
+        sp = r.spec
+        d_el = sp.n * sp.ch * sp.h * sp.w
+        w_el = sp.m * (sp.ch // r.groups) * sp.r * sp.s
+        g = np.random.default_rng([12203, cfg.cid, li, 61])
+        kind = "row" if g.random() < d_el / (d_el + w_el) else "col"
+        kinds.append(kind)
+        patterns.append(schemes.pattern(kind, sp.n, sp.m, r.lay.E, r.lay.F))
+    # the layerwise choice from each layer's own workflow times (the offline profiling of Sec. 4.3)
+    need = ("CoC+FC/row", "CoC+RC", "CoC+RC+FC", "CoC+FC/col", "CoC+ClC", "CoC+ClC+FC")
+    choice = []
+    for r in runs:
+        sp = r.spec
+        t = schemes.measure(r.lay, r.D, r.W, reps=args.scheme_reps, workflows=need)
+        c = schemes.rc_clc_policy({k: v["us"] for k, v in t.items()}, sp.n * sp.ch * sp.h * sp.w,
+                                  sp.m * (sp.ch // r.groups) * sp.r * sp.s)
+        choice.append((c.rc_on, c.clc_on))
+    policies = {"rc_clc_off": [ft.make_policy(rc_on=False, clc_on=False)] * nl,
+                "layerwise": [ft.make_policy(rc_on=a, clc_on=b) for a, b in choice]}
+
+    def evp():
+        return (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+
+    def step(pols, fl):
+        for li, r in enumerate(runs):
+            r.lay.policy = pols[li]
+            r.lay.conv_sums(r.D, r.W, r.O, patterns[li] if li == fl else (), encode=True)
+            r.lay.verify_correct_sums(r.D, r.W, r.O, coc=True)
+
+    def plain():
+        for r in runs:
+            r.lay.conv_ws(r.D, r.W, r.O)
+
+    for _ in range(2):
+        step(policies["layerwise"], -1)
+        plain()
+    torch.cuda.synchronize()
+    # the outcome of every epoch, untimed: the faulted layer corrected, every other layer clean
+    outcome = {k: [None] * nl for k in policies}
+    ok = True
+    for k, pols in policies.items():
+        for i in range(nl):
+            step(pols, i)
+            rep = runs[i].lay.read_report()
+            used = sorted({schemes.SCHEME_NAMES.get(fx[4], str(fx[4])) for fx in rep.fixes})
+            outcome[k][i] = {"status": rep.status, "schemes": used}
+            ok = ok and rep.status == ft.STATUS_CORRECTED and all(
+                not runs[j].lay.read_report().detected for j in range(nl) if j != i)
+    # timed: per round, every epoch of both policies, the error-free step and the unprotected one,
+    # queued back to back with events between them (no host wait inside a round)
+    times = {"unprotected": [], "error_free": []}
+    epoch_ms = {k: [[] for _ in range(nl)] for k in policies}
+    for _ in range(args.protocol_rounds):
+        marks = []
+        for k, pols in policies.items():
+            for i in range(nl):
+                a, b = evp()
+                a.record()
+                step(pols, i)
+                b.record()
+                marks.append((k, i, a, b))
+            for v in ("error_free", "unprotected"):
+                a, b = evp()
+                a.record()
+                if v == "error_free":
+                    step(pols, -1)
+                else:
+                    plain()
+                b.record()
+                marks.append((v, -1, a, b))
+        torch.cuda.synchronize()
+        for k, i, a, b in marks:
+            if i >= 0:
+                epoch_ms[k][i].append(a.elapsed_time(b))
+            else:
+                times[k].append(a.elapsed_time(b))
+    base = statistics.median(times["unprotected"])
+    free = statistics.median(times["error_free"])
+    out = {"mode": "fault_protocol", "workload": cfg.name, "layers": nl, "rounds": args.protocol_rounds,
+           "unprotected_ms": round(base, 4), "error_free_ms": round(free, 4),
+           "overhead_error_free_pct": round((free / base - 1) * 100, 2),
+           "patterns": {"row": kinds.count("row"), "col": kinds.count("col")}}
+    for k in policies:
+        med = [statistics.median(x) for x in epoch_ms[k]]
+        mean = sum(med) / nl
+        used = {}
+        for o in outcome[k]:
+            for sname in o["schemes"]:
+                used[sname] = used.get(sname, 0) + 1
+        out[k] = {"mean_epoch_ms": round(mean, 4), "overhead_pct": round((mean / base - 1) * 100, 2),
+                  "correction_pct": round((mean / free - 1) * 100, 2),
+                  "resolved_by": used,
+                  "per_layer": [{"layer": runs[i].name, "pattern": kinds[i], "ms": round(med[i], 4),
+                                 "extra_us": round((med[i] - free) * 1e3, 1), **outcome[k][i]}
+                                for i in range(nl)]}
+    out["layerwise"]["rc_on_layers"] = sum(1 for a, _ in choice if a)
+    out["layerwise"]["clc_on_layers"] = sum(1 for _, b in choice if b)
+    out["all_corrected"] = bool(ok)
+    print(json.dumps(out), flush=True)
+    return 0 if ok else 1
+
+
 def kernel_key(ft, lay, path=1):
     """The convolution kernel a layer launches (ftcnn_conv_tile): layers with the same key run the
     same kernel instantiation."""
@@ -232,6 +356,8 @@ def main():
     if args.schemes:
         scheme_table(args, cfg, runs, ft, torch)
         return
+    if args.fault_protocol:
+        return fault_protocol(args, cfg, runs, ft, torch)
     if args.chain:
         return chain_bench(args, cfg, runs, ft, torch)
     dtype = cfg.layers[0].dtype

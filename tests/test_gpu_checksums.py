@@ -107,3 +107,30 @@ def test_integer_checksums_exact():
     np.testing.assert_array_equal(b["co5"], b["so5"])
     np.testing.assert_array_equal(b["co6"], b["so6"])
     np.testing.assert_array_equal(b["co7"], b["so7"])
+
+
+def test_co6_alone_needs_no_cw1():
+    """Co6 = Cd1 (x) Cw2 (Sec. 3.2) reads Cd1 and Cw2 only: asked for alone with ck->cw1 NULL,
+    ftcnn_checksum_conv computes it without touching Cw1, and Co5/Co7 stay untouched."""
+    spec = SHAPES[2]
+    cfg = _cfg_for(spec)
+    D, W = wl.gen_d(cfg, 0, spec), wl.gen_w(cfg, 0, spec)
+    lay = layer_for(spec)
+    Dd, Wd = dev(D, spec.dtype), dev(W, spec.dtype)
+    lay.encode_weights(Wd)
+    lay.encode_input(Dd)
+    for k in ("co5", "co6", "co7"):
+        lay.buf[k].fill_(-7.0)
+    ck = ft._lib.Checksums()
+    for k, t in lay.buf.items():
+        setattr(ck, k, t.data_ptr())
+    ck.cw1 = None
+    ft.checksum_conv(lay.desc, ft.CO6, None, None, ck)
+    torch.cuda.synchronize()
+    cd1, cd2 = wf.encode(D, 0)
+    cw1, cw2 = wf.encode(W, 0)
+    c = wf.Checksums(cd1, cd2, cw1, cw2)
+    wf.coc_checksums(c, spec.stride, spec.pad)
+    got = lay.buf["co6"].cpu().numpy().reshape(c.co6.shape)
+    assert_close_scaled(got, c.co6, 1e-11, "co6")
+    assert (lay.buf["co5"] == -7.0).all() and (lay.buf["co7"] == -7.0).all()
