@@ -457,7 +457,10 @@ def main():
     # path, so that a drift of the clock over the run falls on all of them alike; per-step events
     # give medians and percentiles, per-layer events (error-free and unprotected) the per-layer
     # overheads from the same steps
-    variants = ["erroneous", "error_free", "unprotected", "separate"]
+    # The per-layer events sit in steps of their own ("..._layers"): an event between layers costs
+    # a few microseconds of the stream, which would otherwise weigh on the small-layer workloads'
+    # aggregates.
+    variants = ["erroneous", "error_free", "unprotected", "separate", "error_free_layers", "unprotected_layers"]
     per = max(2, args.steps // 4)
     rounds = 4
     steps_ms = {v: [] for v in variants}
@@ -465,25 +468,26 @@ def main():
     for _ in range(rounds):
         for v in variants:
             evs = [evp() for _ in range(per)]
-            lev = [[evp() for _ in runs] for _ in range(per)] if v in lay_ms else None
+            lev = [[evp() for _ in runs] for _ in range(per)] if v.endswith("_layers") else None
             torch.cuda.synchronize()
             for i in range(per):
                 evs[i][0].record()
                 if v == "erroneous":
                     protected_step(i, True)
-                elif v == "error_free":
-                    protected_step(i, False, lay_ev=lev[i])
-                elif v == "unprotected":
-                    conv_step(i, lay_ev=lev[i])
+                elif v.startswith("error_free"):
+                    protected_step(i, False, lay_ev=lev[i] if lev else None)
+                elif v.startswith("unprotected"):
+                    conv_step(i, lay_ev=lev[i] if lev else None)
                 else:
                     separate_step(i)
                 evs[i][1].record()
             torch.cuda.synchronize()
             steps_ms[v] += [a.elapsed_time(b) for a, b in evs]
             if lev is not None:
+                base = v[:-len("_layers")]
                 for i in range(per):
                     for li in range(nl):
-                        lay_ms[v][li].append(lev[i][li][0].elapsed_time(lev[i][li][1]))
+                        lay_ms[base][li].append(lev[i][li][0].elapsed_time(lev[i][li][1]))
     med = {v: q(steps_ms[v], 50) for v in variants}
 
     # ---- cold caches: each layer alone after a 512 MiB write (twice the 256 MB last-level
@@ -578,11 +582,15 @@ def main():
         "overhead_error_free_pct": round((med["error_free"] / med["unprotected"] - 1) * 100, 2),
         "overhead_erroneous_pct": round((med["erroneous"] / med["unprotected"] - 1) * 100, 2),
         "variants_step_ms": {v: stats_ms(steps_ms[v]) for v in variants},
-        "overhead_timing": f"medians of per-step events; the four variants in {rounds} rounds of turns of "
+        "overhead_timing": f"medians of per-step events; the variants in {rounds} rounds of turns of "
                            f"{per} steps after the timed region; per-layer times from events between the "
-                           "layers of the same error-free and unprotected steps",
+                           "layers of the error-free and unprotected steps of the same rounds "
+                           "(variants ..._layers: those steps carry the per-layer events, the others none)",
         "per_layer_sum_ms": {"error_free": round(sum_prot, 4), "unprotected": round(sum_plain, 4),
-                             "overhead_pct": round((sum_prot / sum_plain - 1) * 100, 2)},
+                             "overhead_pct": round((sum_prot / sum_plain - 1) * 100, 2),
+                             "steps_with_layer_events_ms": {
+                                 "error_free": round(med["error_free_layers"], 4),
+                                 "unprotected": round(med["unprotected_layers"], 4)}},
         "cold_cache": {"error_free_ms": round(sum_cprot, 4), "unprotected_ms": round(sum_cplain, 4),
                        "overhead_error_free_pct": round((sum_cprot / sum_cplain - 1) * 100, 2),
                        "note": f"each layer alone after a 512 MiB write, median of {cold_reps}; sums over the "
