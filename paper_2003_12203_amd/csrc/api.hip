@@ -63,6 +63,10 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
         (long long)d->n * d->m > (1LL << 30) || (long long)d->n * CHW >= (1LL << 31) ||
         (long long)d->m * K >= (1LL << 31))
         return fail(FTCNN_E_SHAPE, "dimension beyond the supported range");
+    // the bf16 epilogue adds the weighted terms (m + wbase) o of a pixel in fp32 runs; they are exact
+    // (8-bit significands times weights below 2^16), which bounds the runs' rounding
+    if (d->dtype == FTCNN_BF16 && (long long)d->m + d->wbase > (1LL << 16))
+        return fail(FTCNN_E_UNSUPPORTED, "bf16 layers take at most 65536 - wbase filters");
     g.K = (int)K;
     g.EF = (int)EF;
     g.CHW = CHW;

@@ -79,6 +79,18 @@ def test_bad_descriptor(kw, code):
     assert ft.last_error()
 
 
+def test_bf16_filter_count_bound():
+    """The bf16 epilogue's fp32 runs are exact only while every weight m + wbase stays within
+    2^16: 65536 filters pass with wbase 0, not with wbase 1; fp32 layers have no such bound."""
+    ok = ft.make_desc(1, 1, 4, 4, 65536, 1, 1, dtype="bf16")
+    assert ft.out_shape(ok) == (4, 4)
+    over = ft.make_desc(1, 1, 4, 4, 65536, 1, 1, dtype="bf16", wbase=1)
+    E, F = C.c_int32(), C.c_int32()
+    assert _lib.load().ftcnn_out_shape(C.byref(over), C.byref(E), C.byref(F)) == -6
+    assert "65536" in ft.last_error()
+    assert ft.out_shape(ft.make_desc(1, 1, 4, 4, 65537, 1, 1, dtype="f32")) == (4, 4)
+
+
 def test_grouped_descriptor_accepted():
     d = ft.make_desc(2, 4, 8, 8, 6, 3, 3, groups=2)
     assert ft.out_shape(d) == (6, 6)
