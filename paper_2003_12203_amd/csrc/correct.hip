@@ -882,16 +882,16 @@ __device__ __attribute__((always_inline)) void fresh_range(const Ctx<T> &c, int 
 // Whether this workgroup is the last of the launch to get here (every workgroup calls it once):
 // its own group's counter first, and the last of each group in the top counter.  Every store the
 // stage publishes is thread 0's, so thread 0's fence makes them visible to the last workgroup.
-__device__ inline bool last_to_finish(int *done, Sh &sh) {
+__device__ inline bool last_to_finish(int *done, Sh &sh, int blk, int nblk) {
     __syncthreads();
     if (threadIdx.x == 0) {
         __threadfence();
-        const int grp = (int)(blockIdx.x % kDoneGroups);
-        const int members = ((int)gridDim.x - grp + kDoneGroups - 1) / kDoneGroups;
+        const int grp = blk % kDoneGroups;
+        const int members = (nblk - grp + kDoneGroups - 1) / kDoneGroups;
         int last = 0;
         if (atomicAdd(&done[kDoneStride * (1 + grp)], 1) == members - 1) {
             __threadfence();
-            const int groups = (int)gridDim.x < kDoneGroups ? (int)gridDim.x : kDoneGroups;
+            const int groups = nblk < kDoneGroups ? nblk : kDoneGroups;
             last = atomicAdd(&done[0], 1) == groups - 1;
         }
         sh.slot = last;
@@ -901,9 +901,21 @@ __device__ inline bool last_to_finish(int *done, Sh &sh) {
     return sh.slot != 0;
 }
 
+// The wide stage as workgroup blk of nblk (a launch of its own, or the helpers of the fused final
+// launch).
+struct WideArgs {
+    unsigned char *corr;
+    CorrLayout L;
+    size_t stride;
+    int use_win, cache_rows;
+};
+
 template <typename T>
-__global__ __launch_bounds__(kThreads) void wide_kernel(Ctx<T> c, unsigned char *corr, CorrLayout L, size_t stride,
-                                                        int use_win, int cache_rows) {
+__device__ __attribute__((always_inline)) void wide_body(Ctx<T> c, const WideArgs &wa, int blk, int nblk) {
+    unsigned char *corr = wa.corr;
+    const CorrLayout &L = wa.L;
+    const size_t stride = wa.stride;
+    const int use_win = wa.use_win, cache_rows = wa.cache_rows;
     const int np = min(c.rep->reserved[0], c.g.EF);
     if (np <= 0) return;
     __shared__ Sh sh;
@@ -914,7 +926,7 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(Ctx<T> c, unsigned char 
     double *fresh = reinterpret_cast<double *>(corr + L.fresh);
     int *done = reinterpret_cast<int *>(corr + L.done);
     const int nb = min(np, kMaxPending);
-    bind_scratch(c, reinterpret_cast<double *>(corr + L.chain) + stride * blockIdx.x);
+    bind_scratch(c, reinterpret_cast<double *>(corr + L.chain) + stride * blk);
     for (int m = threadIdx.x; m < g.M; m += kThreads) c.colmark[m] = 0;
     // the window of the position whose filters this workgroup is on (shared memory, when it fits)
     extern __shared__ double win_sm[];
@@ -925,21 +937,21 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(Ctx<T> c, unsigned char 
     // checksum ranges
     const int pu = position_units(g), nf = filter_units(g);
     const long long total = (long long)nb * pu;
-    const long long run = (total + gridDim.x - 1) / gridDim.x;
-    for (long long it = (long long)blockIdx.x * run; it < total && it < (long long)(blockIdx.x + 1) * run; ++it) {
+    const long long run = (total + nblk - 1) / nblk;
+    for (long long it = (long long)blk * run; it < total && it < (long long)(blk + 1) * run; ++it) {
         const int q = (int)(it / pu), u = (int)(it - (long long)q * pu);
         const int p = pend[q].p;
         const bool stage = win.c1 && u < nf && staged != q;
         if (stage) staged = q;
         run_unit(c, sh, p, u, stage, rows + (size_t)q * g.M * kRowSums, cols + (size_t)q * g.N * kColSums, win);
     }
-    for (int q = 0; q < nb && blockIdx.x < kFreshRanges; ++q) {
+    for (int q = 0; q < nb && blk < kFreshRanges; ++q) {
         if (pend[q].mode != 1) continue;
         const int p = pend[q].p, x = p / g.F;
         double v[3];
-        fresh_range(c, x, p - x * g.F, blockIdx.x, sh, v);
+        fresh_range(c, x, p - x * g.F, blk, sh, v);
         if (threadIdx.x == 0) {
-            double *f = fresh + ((size_t)q * kFreshRanges + blockIdx.x) * 3;
+            double *f = fresh + ((size_t)q * kFreshRanges + blk) * 3;
             f[0] = v[0];
             f[1] = v[1];
             f[2] = v[2];
@@ -947,12 +959,12 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(Ctx<T> c, unsigned char 
     }
     // then the positions past the shared batch, one workgroup each on its own slabs; the last
     // workgroup to finish (a completion counter, no waiting) then takes the shared batch's decisions
-    double *myrows = rows + (size_t)(kMaxPending + blockIdx.x) * g.M * kRowSums;
-    double *mycols = cols + (size_t)(kMaxPending + blockIdx.x) * g.N * kColSums;
+    double *myrows = rows + (size_t)(kMaxPending + blk) * g.M * kRowSums;
+    double *mycols = cols + (size_t)(kMaxPending + blk) * g.N * kColSums;
     bool batch = false;
-    for (int q = kMaxPending + blockIdx.x;; q += batch ? 1 : (int)gridDim.x) {
+    for (int q = kMaxPending + blk;; q += batch ? 1 : nblk) {
         if (!batch && q >= np) {
-            if (!last_to_finish(done, sh)) return;
+            if (!last_to_finish(done, sh, blk, nblk)) return;
             batch = true;
             q = 0;
         }
@@ -1017,6 +1029,11 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(Ctx<T> c, unsigned char 
     if (threadIdx.x == 0) c.rep->reserved[0] = 0;
 }
 
+template <typename T>
+__global__ __launch_bounds__(kThreads) void wide_kernel(Ctx<T> c, WideArgs wa) {
+    wide_body(c, wa, (int)blockIdx.x, (int)gridDim.x);
+}
+
 // Co5 = Cd1 (x) Cw1, Co6 = Cd1 (x) Cw2, Co7 = Cd2 (x) Cw1 at position (x, y)
 // (Sec. 3.2): this lane's share of the K taps, k = lane, lane + TPP, ...,
 // with (ch, r, s) advanced incrementally.
@@ -1072,20 +1089,31 @@ __device__ inline void coc_taps(const Ctx<T> &c, int lane, int x, int y, double 
 // positions (thread t: position t % per, lane t / per), so every load of a
 // partial slice is a coalesced run; the lanes of a position are then added in a
 // fixed order (exchanges inside each wave, then the four waves).
+struct DetectArgs {
+    int splits, max_groups;
+    const double *part, *copart;
+    double *co5, *co6, *co7, *so5, *so6, *so7, *q5;
+    int *flags;
+    Pending *pend;
+    int *wide_done;
+};
+
+// Detection block blk.
 template <typename T, int TPP, bool COC>
-__global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int splits, const double *__restrict__ part,
-                                                                  const double *__restrict__ copart, int max_groups,
-                                                                  double *co5, double *co6, double *co7,
-                                                                  double *so5, double *so6, double *so7, double *q5,
-                                                                  int *__restrict__ flags, Pending *pend,
-                                                                  int *wide_done) {
-    if (blockIdx.x == 0 && threadIdx.x <= kDoneGroups) wide_done[kDoneStride * threadIdx.x] = 0;  // the wide stage's count
+__device__ __attribute__((always_inline)) void detect_block(const Ctx<T> &c, const DetectArgs &da, int blk) {
+    const int splits = da.splits, max_groups = da.max_groups;
+    const double *__restrict__ part = da.part;
+    const double *__restrict__ copart = da.copart;
+    double *co5 = da.co5, *co6 = da.co6, *co7 = da.co7, *so5 = da.so5, *so6 = da.so6, *so7 = da.so7, *q5 = da.q5;
+    int *__restrict__ flags = da.flags;
+    Pending *pend = da.pend;
+    if (blk == 0 && threadIdx.x <= kDoneGroups) da.wide_done[kDoneStride * threadIdx.x] = 0;  // the wide stage's count
     constexpr int NV = COC ? 7 : 4;
     __shared__ double red[TPP > 1 ? NV : 1][TPP > 1 ? 4 * (kThreads / TPP) : 1];
     const Geom &g = c.g;
     constexpr int per = kThreads / TPP;
     const int slot = threadIdx.x % per, lane = threadIdx.x / per;
-    const int p = blockIdx.x * per + slot;
+    const int p = blk * per + slot;
     double v[NV];
 #pragma unroll
     for (int i = 0; i < NV; ++i) v[i] = 0.0;
@@ -1191,6 +1219,11 @@ __global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, int 
     }
 }
 
+template <typename T, int TPP, bool COC>
+__global__ __launch_bounds__(kThreads) void verify_correct_kernel(Ctx<T> c, DetectArgs da) {
+    detect_block<T, TPP, COC>(c, da, (int)blockIdx.x);
+}
+
 template <typename T>
 Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums &ck,
                 const ftcnn_policy &pol, ftcnn_report *rep) {
@@ -1215,19 +1248,28 @@ Ctx<T> make_ctx(const Plan &pl, const void *D, const void *W, void *O, const ftc
     return c;
 }
 
+// The wide stage's launch arguments: the window of a position, and the decisions' per-filter sums,
+// in shared memory when they fit beside a second workgroup's.
+inline WideArgs wide_args(const Plan &pl, void *ws, size_t *lds) {
+    WideArgs wa;
+    wa.corr = static_cast<unsigned char *>(ws) + pl.off_corr;
+    wa.L = corr_layout(pl.g, pl.corr_stride);
+    wa.stride = pl.corr_stride;
+    const size_t win_bytes = (2 * sizeof(double) + 1) * (size_t)pl.g.K;
+    const size_t row_bytes = sizeof(double) * kRowSums * (size_t)pl.g.M;
+    wa.use_win = win_bytes <= kWindowBytes;
+    wa.cache_rows = row_bytes <= kWindowBytes;
+    *lds = std::max(wa.use_win ? win_bytes : 0, wa.cache_rows ? row_bytes : 0);
+    return wa;
+}
+
 // The wide stage after a flagging launch: wide_grid workgroups that return at once unless
 // positions were handed over.
 template <typename T>
 hipError_t launch_wide(const Plan &pl, const Ctx<T> &c, void *ws, hipStream_t st) {
-    unsigned char *corr = static_cast<unsigned char *>(ws) + pl.off_corr;
-    // the window of a position, and the decisions' per-filter sums, in shared memory when they fit
-    // beside a second workgroup's
-    const size_t win_bytes = (2 * sizeof(double) + 1) * (size_t)pl.g.K;
-    const size_t row_bytes = sizeof(double) * kRowSums * (size_t)pl.g.M;
-    const int use_win = win_bytes <= kWindowBytes, cache_rows = row_bytes <= kWindowBytes;
-    const size_t lds = std::max(use_win ? win_bytes : 0, cache_rows ? row_bytes : 0);
-    wide_kernel<T><<<(unsigned)wide_grid(pl.g), kThreads, lds, st>>>(
-        c, corr, corr_layout(pl.g, pl.corr_stride), pl.corr_stride, use_win, cache_rows);
+    size_t lds = 0;
+    const WideArgs wa = wide_args(pl, ws, &lds);
+    wide_kernel<T><<<(unsigned)wide_grid(pl.g), kThreads, lds, st>>>(c, wa);
     return hipGetLastError();
 }
 
@@ -1237,23 +1279,23 @@ hipError_t run_fused(const Plan &pl, const void *D, const void *W, void *O, cons
                      hipStream_t st) {
     Ctx<T> c = make_ctx<T>(pl, D, W, O, ck, pol, rep);
     char *w = static_cast<char *>(ws);
-    const double *part = reinterpret_cast<const double *>(w + off_part);
-    int *flags = reinterpret_cast<int *>(w + pl.off_flags);
     const CorrLayout L = corr_layout(pl.g, pl.corr_stride);
-    Pending *pend = reinterpret_cast<Pending *>(w + pl.off_corr + L.pend);
-    int *wide_done = reinterpret_cast<int *>(w + pl.off_corr + L.done);
+    DetectArgs da;
+    da.splits = sp;
+    da.part = reinterpret_cast<const double *>(w + off_part);
+    da.flags = reinterpret_cast<int *>(w + pl.off_flags);
+    da.pend = reinterpret_cast<Pending *>(w + pl.off_corr + L.pend);
+    da.wide_done = reinterpret_cast<int *>(w + pl.off_corr + L.done);
     // Co5..Co7 of a channels-last layer come as partial slices from the convolution launch
     // (the kernel checks rep->reserved[1] and falls back to the taps)
     const int taps = coc ? (pl.co_in_conv ? pl.co.groups * pl.prep_ns : pl.g.K) : 0;
     const int tpp = final_tpp(sp, taps, pl.g.EF);
-    const double *copart = reinterpret_cast<const double *>(w + pl.off_copart);
-    const int max_groups = pl.co_in_conv ? pl.co.groups * pl.prep_ns : 0;
+    da.copart = reinterpret_cast<const double *>(w + pl.off_copart);
+    da.max_groups = pl.co_in_conv ? pl.co.groups * pl.prep_ns : 0;
+    da.co5 = ck.co5; da.co6 = ck.co6; da.co7 = ck.co7;
+    da.so5 = ck.so5; da.so6 = ck.so6; da.so7 = ck.so7; da.q5 = ck.q5;
     const unsigned blocks = (unsigned)((pl.g.EF + kThreads / tpp - 1) / (kThreads / tpp));
-#define VC(TPP, COC)                                                                                            \
-    verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, sp, part, copart, max_groups, ck.co5,       \
-                                                                    ck.co6, ck.co7,                              \
-                                                                    ck.so5, ck.so6, ck.so7, ck.q5, flags, pend,  \
-                                                                    wide_done)
+#define VC(TPP, COC) verify_correct_kernel<T, TPP, COC><<<blocks, kThreads, 0, st>>>(c, da)
     if (coc) {
         if (tpp == 1) VC(1, true);
         else if (tpp == 4) VC(4, true);
