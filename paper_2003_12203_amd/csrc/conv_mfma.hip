@@ -1227,8 +1227,22 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
         // grouped layers: rows of tiles inside one group, so that every tile skips the other
         // groups' channels (192 filters a group: 64-row tiles)
         if (g.G > 1 && g.Mg % 128 != 0 && g.Mg % 64 == 0) return f(F32_64x64{});
-        if (n_tiles(g, 128, 128) >= 600) return f(F32_128x128{});
-        if (n_tiles(g, 128, 64) >= 380) return f(F32_128x64{});
+        // the tile with the least predicted time: the padded outputs (tiles x TM x TP), plus half of
+        // the idle slots in the last round of 256 tiles, at the tile's own rate per output
+        // (128 x 128 : 128 x 64 : 64 x 64 = 1 : 0.972 : 0.925).  The one-half and the rates are
+        // fitted to VGG-19 (224^2 .. 14^2, batch 32) and Darknet-19 (104^2 .. 13^2, batch 16),
+        // where they pick the fastest of the three on every layer or one within 1%; 128 x 128
+        // needs at least 600 tiles and 128 x 64 one a compute unit (fewer hide too little latency)
+        const auto cost = [](long long tiles, double tile_outputs, double rate) {
+            const long long slots = (tiles + 255) / 256 * 256;
+            return ((double)tiles + 0.5 * (double)(slots - tiles)) * tile_outputs / rate;
+        };
+        const long long t128 = n_tiles(g, 128, 128), t12864 = n_tiles(g, 128, 64);
+        const double c64 = cost(n_tiles(g, 64, 64), 64.0 * 64.0, 0.925);
+        const double c12864 = t12864 >= 256 ? cost(t12864, 128.0 * 64.0, 0.972) : 1e300;
+        const double c128 = t128 >= 600 ? cost(t128, 128.0 * 128.0, 1.0) : 1e300;
+        if (c128 <= c12864 && c128 <= c64) return f(F32_128x128{});
+        if (c12864 <= c64) return f(F32_128x64{});
         return f(F32_64x64{});
     }
     if (g.M <= 32) return f(BF16_M32{});
