@@ -186,6 +186,16 @@ const char *ftcnn_last_error(void);
  * every kernel a set of layers runs. */
 int ftcnn_conv_tile(const ftcnn_conv_desc *desc, int32_t path, int32_t out[6]);
 
+/* INSTRUMENTATION (host query of the current device, no device work): *workgroups = the
+ * stream-K workgroups of the convolution launched by the calls that take a workspace (path 1
+ * of ftcnn_conv_tile), or 0 when it runs one workgroup per output tile.  Stream-K is a
+ * schedule, not another operation: every workgroup takes an equal run of the layer's
+ * (tile, chunk of K) pairs, and a tile whose chunks span several workgroups is summed by the
+ * last of them to finish, in chunk order (so the protected convolution and its unprotected
+ * twin store the same bits).  It is used for dense channels-last fp32 layers whose tile count
+ * would leave the last round of resident workgroups less than 90 % busy. */
+int ftcnn_conv_stream_k(const ftcnn_conv_desc *desc, int32_t *workgroups);
+
 /* ---- device work -------------------------------------------------------- */
 
 /* Sec. 3.2 input checksums.  which = 0: X is D, c1 = Cd1 = sum_n D_n and

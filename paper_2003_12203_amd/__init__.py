@@ -86,6 +86,14 @@ def conv_tile(desc, path: int = 1) -> dict:
             "group_skip": bool(out[5])}
 
 
+def conv_stream_k(desc) -> int:
+    """ftcnn_conv_stream_k: stream-K workgroups of the layer's workspace-path convolution on the
+    current device (0: one workgroup per tile)."""
+    out = C.c_int32(0)
+    _check(lib().ftcnn_conv_stream_k(C.byref(desc), C.byref(out)), "ftcnn_conv_stream_k")
+    return int(out.value)
+
+
 def last_error() -> str:
     return lib().ftcnn_last_error().decode(errors="replace")
 

@@ -58,7 +58,7 @@ EXPORTS = ("ftcnn_out_shape", "ftcnn_workspace_bytes", "ftcnn_report_bytes", "ft
            "ftcnn_verify_correct", "ftcnn_conv_fwd_ws", "ftcnn_conv_fwd_sums", "ftcnn_verify_correct_sums", "ftcnn_protected_conv",
            "ftcnn_inject", "ftcnn_set_kernel_events", "ftcnn_conv_fwd_bias", "ftcnn_check_weights",
            "ftcnn_relu_pool", "ftcnn_relu_pool_encode", "ftcnn_conv_fwd_sums_given", "ftcnn_conv_tile",
-           "ftcnn_protected_conv_noalloc")
+           "ftcnn_protected_conv_noalloc", "ftcnn_conv_stream_k")
 
 _lib = None
 
@@ -81,6 +81,8 @@ def load(path: str = LIB_PATH):
     L.ftcnn_report_bytes.restype = C.c_size_t
     L.ftcnn_conv_tile.argtypes = [P(ConvDesc), C.c_int32, P(C.c_int32)]
     L.ftcnn_conv_tile.restype = C.c_int
+    L.ftcnn_conv_stream_k.argtypes = [P(ConvDesc), P(C.c_int32)]
+    L.ftcnn_conv_stream_k.restype = C.c_int
     L.ftcnn_last_error.argtypes = []
     L.ftcnn_last_error.restype = C.c_char_p
     L.ftcnn_encode.argtypes = [P(ConvDesc), C.c_int32, _dp, _dp, _dp, _dp, _dp]

@@ -40,7 +40,7 @@ int row_splits(long long rows, long long col_blocks, long long target_blocks, lo
 
 // allow_nhwc = false: every convolution gathers from D as given (no channels-last copies in
 // the workspace), a plan with a smaller workspace for layers that would otherwise copy.
-int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
+int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true, bool allow_sk = true) {
     if (!d) return fail(FTCNN_E_ARG, "null descriptor");
     if (d->groups < 1 || d->ch % d->groups != 0 || d->m % d->groups != 0)
         return fail(FTCNN_E_SHAPE, "groups = %d must divide ch = %d and m = %d", d->groups, d->ch, d->m);
@@ -169,6 +169,25 @@ int make_plan(const ftcnn_conv_desc *d, Plan *pl, bool allow_nhwc = true) {
     off += align256(2 * sizeof(double) * (size_t)K);
     pl->off_wfull = off;  // grouped layers: the block-diagonal expansion of W
     off += g.G > 1 ? align256((size_t)g.M * K * es) : 0;
+    // the stream-K partials and per-tile counts of the channels-last convolution (the counts are
+    // cleared by the channels-last copy that runs before every such convolution)
+    pl->sk_smax = 0;
+    pl->sk_counters = 0;
+    pl->off_skpart = pl->off_skcnt = off;
+    if (pl->nhwc && allow_sk) {
+        int smax = 0;
+        size_t pbytes = 0;
+        long long counters = 0;
+        conv_sk_space(g, true, &smax, &pbytes, &counters);
+        if (smax > 0) {
+            pl->sk_smax = smax;
+            pl->sk_counters = counters;
+            pl->off_skpart = off;
+            off += align256(pbytes);
+            pl->off_skcnt = off;
+            off += align256((size_t)counters * sizeof(int));
+        }
+    }
     pl->bytes = off;
     return FTCNN_OK;
 }
@@ -417,6 +436,14 @@ int ftcnn_conv_tile(const ftcnn_conv_desc *desc, int32_t path, int32_t out[6]) {
     return FTCNN_OK;
 }
 
+int ftcnn_conv_stream_k(const ftcnn_conv_desc *desc, int32_t *workgroups) {
+    Plan pl;
+    FT_TRY(make_plan(desc, &pl));
+    if (!workgroups) return fail(FTCNN_E_ARG, "conv_stream_k: null output");
+    *workgroups = conv_stream_k(pl);
+    return FTCNN_OK;
+}
+
 size_t ftcnn_report_bytes(int32_t cap_fixes) {
     return sizeof(ftcnn_report) + (size_t)(cap_fixes > 0 ? cap_fixes : 0) * sizeof(ftcnn_fix);
 }
@@ -474,11 +501,13 @@ int ftcnn_protected_conv(const ftcnn_conv_desc *desc, const void *D, const void 
 int ftcnn_protected_conv_noalloc(const ftcnn_conv_desc *desc, const void *D, const void *W, void *O,
                                  const ftcnn_checksums *ck, const ftcnn_policy *policy, ftcnn_report *rep,
                                  int32_t cap_fixes, hipStream_t stream) {
-    // the plan of ftcnn_protected_conv when its workspace fits the static scratch, else the plan
-    // without channels-last copies (a smaller workspace, the same results within the output
-    // tolerance: K is summed in (c, r, s) order instead of (r, s, c))
+    // the plan of ftcnn_protected_conv when its workspace fits the static scratch, else that plan
+    // without the stream-K scratch (whole tiles per workgroup: K split at other places), else the
+    // plan without channels-last copies (K summed in (c, r, s) order instead of (r, s, c)); the
+    // last two give the same results within the output tolerance
     Plan pl;
     FT_TRY(make_plan(desc, &pl));
+    if (pl.bytes > kStaticScratchBytes) FT_TRY(make_plan(desc, &pl, true, false));
     if (pl.bytes > kStaticScratchBytes) {
         FT_TRY(make_plan(desc, &pl, false));
         if (pl.bytes > kStaticScratchBytes)

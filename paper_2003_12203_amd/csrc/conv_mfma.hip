@@ -316,6 +316,11 @@ struct TapWalk {
     }
     __device__ inline int kb(const Geom &g) const { return (r * g.S + s) * g.C + c0; }
 };
+// The TapWalk state of chunk j (chunks of tk channels, channel blocks outer, taps inner).
+__device__ inline TapWalk tap_at(const Geom &g, int j, int tk) {
+    const int rs_n = g.R * g.S, blk = j / rs_n, rs = j - blk * rs_n, r = rs / g.S;
+    return TapWalk{r, rs - r * g.S, blk * tk};
+}
 
 // A 16-byte unit in global memory (address space 1): loads through it are global loads that the
 // compiler knows cannot alias the thread's private arrays, which then stay in registers.
@@ -530,7 +535,7 @@ template <int NI, int STAGES> __device__ inline void wait_chunks_behind(int behi
 template <typename C, int FM, int FP, int STAGES>
 __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom &g, int m0, long long p0,
                                     const unsigned char *zp_dt, unsigned char *smem, floatx16 (&acc)[FM][FP],
-                                    int tid, int arow0, int brow0) {
+                                    int tid, int arow0, int brow0, int k0, int kn) {
     constexpr int NW = C::NT / 64;
     constexpr int NIA = C::TM / (8 * NW), NIB = C::TP / (8 * NW), NI = NIA + NIB;
     static_assert(C::TM % (8 * NW) == 0 && C::TP % (8 * NW) == 0 && (STAGES - 1) * NI < 64, "DMA tile shape");
@@ -578,8 +583,9 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
             buffer_load_lds16(rd, base + STAGE_A + (j * NW + w) * 8 * 128, ok ? b_off[j] + tap : 0u, 0u);
         }
     };
-    const int nch = g.R * g.S * (g.C / 64);
-    TapWalk ti{0, 0, 0};
+    // chunks [k0, k0 + nch) of the tile's K (kn < 0: all of them)
+    const int nch = kn >= 0 ? kn : g.R * g.S * (g.C / 64);
+    TapWalk ti = tap_at(g, k0, 64);
 #pragma unroll
     for (int st = 0; st + 1 < STAGES; ++st) {
         if (st < nch) {
@@ -620,6 +626,19 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
 //               channels-last copy, and compute the Co5..Co7 partial products
 //               (coc_tile.h).
 struct NoFaults {};
+// Stream-K schedule of the channels-last and direct-to-LDS loops (S > 0): the launch has S
+// workgroups (after the extra ones), and workgroup w runs the iterations [w U / S, (w + 1) U / S)
+// of the U = tiles x nch (tile, chunk) pairs in tile order, so every workgroup gets the same
+// share of matrix work whatever the tile count.  A tile whose chunks span several workgroups is
+// summed by the last of them to arrive: each writes its partial accumulators to a slot (0: the
+// workgroup's first segment, 1: its last), counts itself in cnt[tile], and the last adds the
+// slots in chunk order (a fixed order, whichever workgroup is last) before the epilogue.
+struct SkArgs {
+    float *part;   // [S][2][TM * TP]
+    int *cnt;      // [tiles], zero at the launch (the channels-last copy clears it); left zero
+    int S;         // 0: one tile per workgroup
+    int nch;       // chunks per tile
+};
 template <int EPI> struct Epi {
     double *part;
     ftcnn_report *rep;
@@ -651,12 +670,13 @@ template <> struct Bits<uint16_t> {
     __device__ static float value(B b) { return bf16_bits_to_f32(b); }
 };
 
-template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC, bool GRP = false>
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC, bool GRP = false,
+          bool SK = false>
 __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T *__restrict__ D,
                                                             const typename Tr::T *__restrict__ Wt,
                                                             typename Tr::T *__restrict__ O, Geom g,
                                                             int tiles_m, int tiles_total, int m_major,
-                                                            const void *zp, Epi<EPI> ep) {
+                                                            const void *zp, Epi<EPI> ep, SkArgs sk) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC, (WEAVE >= 3 ? WEAVE - 1 : 0)>;
     using T = typename C::T;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -686,15 +706,57 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                 return;
             }
             bid -= 8 * ep.aux_groups;   // keeps bid % 8, hence the XCD the tile order assumes
-            if (bid >= tiles_total) return;
         }
+    }
+    constexpr bool DMA = NHWC && WEAVE >= 3 && sizeof(T) == 2 && C::TK == 64;
+    // the stream-K form (a separate kernel: the whole-tile kernels keep their registers) of the
+    // loops that can run a range of a tile's chunks (channels-last, dense)
+    constexpr bool SKOK = SK && NHWC && !GRP && WEAVE != 2;
+    constexpr bool skm = SKOK;
+    long long sk_it = 0, sk_end = 0, sk_u = 0;
+    int wl = 0;
+    if (skm) {
+        if (bid >= sk.S) return;
+        // contiguous iteration ranges per XCD, as the tile order below
+        wl = xcd_tile(bid, sk.S);
+        sk_u = (long long)tiles_total * sk.nch;
+        sk_it = (long long)wl * sk_u / sk.S;
+        sk_end = (long long)(wl + 1) * sk_u / sk.S;
+    } else if (bid >= tiles_total) {
+        return;
+    }
+    bool first_seg = true;
+    const Geom &g_all = g;
+    for (;;) {
+    // In the stream-K kernel the thread index and the geometry are passed through empty asm at
+    // every segment, so that nothing derived from them is hoisted out of the segment loop and
+    // held (in registers, or spilled) across the main loop and the epilogue.
+    int tid;
+    Geom g = g_all;
+    if constexpr (SK) {
+        asm volatile("v_mov_b32 %0, %1" : "=v"(tid) : "v"((int)threadIdx.x));
+        asm volatile("" : "+s"(g.N), "+s"(g.C), "+s"(g.H), "+s"(g.W), "+s"(g.M), "+s"(g.R), "+s"(g.S));
+        asm volatile("" : "+s"(g.U), "+s"(g.P), "+s"(g.E), "+s"(g.F), "+s"(g.K), "+s"(g.EF));
+        asm volatile("" : "+s"(g.CHW), "+s"(g.P_total), "+s"(g.wbase));
+    } else {
+        tid = threadIdx.x;
     }
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wp = wave / WM;
-    // logical tile order: pixel-major keeps the M tiles of one pixel tile on one
-    // XCD (its L2 serves the repeated D reads); M-major keeps one slab of W
-    // resident per XCD instead (preferred when W is larger than an XCD's L2)
-    const int tile = xcd_tile(bid, tiles_total);
+    // the segment: chunks [k0, k0 + kn) of one tile (kn < 0: the whole tile)
+    int tile, k0 = 0, kn = -1;
+    if (skm) {
+        if (sk_it >= sk_end) break;
+        tile = (int)(sk_it / sk.nch);
+        k0 = (int)(sk_it - (long long)tile * sk.nch);
+        kn = (int)(sk_end - sk_it < (long long)(sk.nch - k0) ? sk_end - sk_it : (long long)(sk.nch - k0));
+        if (!first_seg) __syncthreads();   // every wave is done with the last segment's LDS
+    } else {
+        // logical tile order: pixel-major keeps the M tiles of one pixel tile on one
+        // XCD (its L2 serves the repeated D reads); M-major keeps one slab of W
+        // resident per XCD instead (preferred when W is larger than an XCD's L2)
+        tile = xcd_tile(bid, tiles_total);
+    }
     const int tiles_p = tiles_total / tiles_m;
     const int mt = m_major ? tile / tiles_p : tile % tiles_m;
     const int pt = m_major ? tile % tiles_p : tile / tiles_m;
@@ -727,7 +789,6 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
     const int arow0 = wm * FM * 32, brow0 = wp * FP * 32;
-    constexpr bool DMA = NHWC && WEAVE >= 3 && sizeof(T) == 2 && C::TK == 64;
     Pack<T, C::VEC> ra[C::A_PER];
     Pack<T, C::VEC> rb[C::KR / C::VEC];
     const int nchunks = (g.K + C::TK - 1) / C::TK;
@@ -762,6 +823,10 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         tw.c0 = cg0;
         if (!(KSKIP && cpr > 0)) nch = g.R * g.S * (g.C / C::TK);
         pix_off = lane_base + (ih0 * g.W + iw0) * g.C + bkg * C::KR;
+        if (SKOK && kn >= 0) {
+            tw = tap_at(g, k0, C::TK);
+            nch = kn;
+        }
     }
     if constexpr (!DMA) {
         if constexpr (TAPS) {
@@ -779,7 +844,8 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     if constexpr (DMA) {
         // D is the channels-last copy, which the workspace keeps right behind the zero page zp
         dma_mainloop<C, FM, FP, WEAVE - 1>(reinterpret_cast<const uint16_t *>(Wt), g, m0, p0,
-                                           static_cast<const unsigned char *>(zp), smem, acc, tid, arow0, brow0);
+                                           static_cast<const unsigned char *>(zp), smem, acc, tid, arow0, brow0,
+                                           k0, kn);
     } else if constexpr (NHWC && WEAVE == 2) {
         // channels-last, two chunks in flight: chunk kc + 2 is loaded into one register set
         // while chunk kc is consumed from LDS, and chunk kc + 1 (loaded a whole chunk earlier,
@@ -890,6 +956,69 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             __syncthreads();
         }
         mma((nchunks - 1) & 1);
+    }
+
+    if constexpr (SKOK) {
+        if (kn >= 0 && kn < sk.nch) {
+            // a part of the tile: publish it; the last of the tile's workgroups sums them all
+            const long long ib = (long long)tile * sk.nch;
+            // the workgroup whose range holds iteration i
+            auto owner = [&](long long i) { return (int)(((i + 1) * sk.S - 1) / sk_u); };
+            const int w0 = owner(ib), w1 = owner(ib + sk.nch - 1);
+            constexpr int NR = FM * FP * 16;   // accumulators per thread; slot layout [NR][NT]
+            float *mine = sk.part + ((size_t)wl * 2 + (first_seg ? 0 : 1)) * (size_t)(C::TM * C::TP);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FP; ++j) {
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        __hip_atomic_store(mine + ((i * FP + j) * 16 + e) * C::NT + tid, acc[i][j][e],
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __builtin_amdgcn_sched_barrier(0);   // a few store addresses live at a time
+                }
+            // The parts go to memory with device-coherent stores (they bypass the XCD's L2), so
+            // once every wave has seen its stores complete, one device-scope count publishes the
+            // whole part: no L2 write-back is needed.  Every wave is past the main loop: the first
+            // word of LDS carries the verdict.
+            int *sk_last = reinterpret_cast<int *>(smem);
+            wait_vmcnt<0>();
+            __syncthreads();
+            if (tid == 0)
+                *sk_last = __hip_atomic_fetch_add(sk.cnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                           w1 - w0;
+            __syncthreads();
+            const bool last = *sk_last != 0;
+            if (!last) {
+                sk_it += kn;
+                first_seg = false;
+                continue;
+            }
+            // the other parts, read with device-coherent loads after the count said they are all there
+            if (tid == 0) __hip_atomic_store(sk.cnt + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // the tile's parts in chunk order (this workgroup's own from its slot too): part w lies
+            // in slot 0 of workgroup w when its range starts inside this tile, else in its slot 1
+            // (its last segment).  Sixteen loads at a time, so the sums need few registers beyond
+            // the accumulators.
+            static_assert(NR * C::NT == C::TM * C::TP, "slot size");
+            for (int w = w0; w <= w1; ++w) {
+                const int slot = (long long)w * sk_u / sk.S >= ib ? 0 : 1;
+                const float *src = sk.part + ((size_t)w * 2 + slot) * (size_t)(C::TM * C::TP) + tid;
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FP; ++j) {
+                        float v[16];
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            v[e] = __hip_atomic_load(src + ((i * FP + j) * 16 + e) * C::NT, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) acc[i][j][e] = w == w0 ? v[e] : acc[i][j][e] + v[e];
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+            }
+        }
     }
 
     // epilogue: lane owns pixel (lane & 31) of each 32-wide block; register e of
@@ -1099,11 +1228,92 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             }
         }
     }
+    if (!skm) break;
+    sk_it += kn;
+    first_seg = false;
+    }   // segments
+}
+
+// Stream-K workgroups of a tile configuration on the current device: the workgroups that are
+// resident at once (the least over the three epilogues, so that the protected kernel and its
+// plain twin split K at the same places and store the same bits), at most smax, a multiple of 8.
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, bool NHWC>
+int sk_workgroups(int smax) {
+    using C = Cfg<Tr, WM, WP, FM, FP, KVEC, (WEAVE >= 3 ? WEAVE - 1 : 0)>;
+    static const int per_cu = [] {
+        int lo = 1 << 30;
+        const void *k[3] = {
+            reinterpret_cast<const void *>(conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, 0, NHWC, false, true>),
+            reinterpret_cast<const void *>(conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, 1, NHWC, false, true>),
+            reinterpret_cast<const void *>(conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, 2, NHWC, false, true>)};
+        const void *w[3] = {
+            reinterpret_cast<const void *>(conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, 0, NHWC>),
+            reinterpret_cast<const void *>(conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, 1, NHWC>),
+            reinterpret_cast<const void *>(conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, 2, NHWC>)};
+        int whole = 1 << 30;
+        size_t spill = 0, spill_whole = 0;
+        for (int i = 0; i < 6; ++i) {
+            const void *f = i < 3 ? k[i] : w[i - 3];
+            if (C::LDS_BYTES > 65536 &&
+                hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES) != hipSuccess)
+                return 0;
+            int nb = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f, C::NT, C::LDS_BYTES) != hipSuccess) return 0;
+            hipFuncAttributes fa;
+            if (hipFuncGetAttributes(&fa, f) != hipSuccess) return 0;
+            if (i < 3) {
+                lo = nb < lo ? nb : lo;
+                spill = fa.localSizeBytes > spill ? fa.localSizeBytes : spill;
+            } else {
+                whole = nb < whole ? nb : whole;
+                spill_whole = fa.localSizeBytes > spill_whole ? fa.localSizeBytes : spill_whole;
+            }
+        }
+        if (spill > spill_whole) return 0;   // registers spilled to scratch: slower than any balance
+        // the stream-K kernels hold more registers; where that costs resident workgroups, the
+        // balance they bring does not pay for it
+        if (lo < whole) return 0;
+        return lo;
+    }();
+    int dev = 0, cus = 0;
+    if (per_cu <= 0 || hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    long long S = (long long)per_cu * cus;
+    S = S < smax ? S : smax;
+    return (int)(S / 8 * 8);
+}
+
+// Stream-K pays (the partial writes and the last workgroup's sums of a split tile) where a plain
+// grid of whole tiles would leave its last round of S resident workgroups partly idle, and where
+// every workgroup still has a long run of chunks.
+inline bool use_stream_k(long long tiles, int S, int nch) {
+    if (tiles * nch < 32LL * S) return false;   // under 32 chunks a workgroup
+    const long long rounds = (tiles + S - 1) / S;
+    return tiles * 100 < rounds * S * 90;       // the whole-tile grid would use < 90 % of its slots
+}
+
+// The stream-K workgroups of a layer's channels-last fp32 convolution on the current device, or 0
+// for one workgroup per tile.  The bf16 loops run whole tiles: on VGG-19 bf16 the stream-K form of
+// the direct-to-LDS 128 x 128 tile was 5-8 % slower where its balance should have helped, and the
+// 256 x 256 tile (eight waves, at most 256 registers each) spills in that form.
+template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, bool NHWC>
+int sk_decide(const Geom &g, int smax) {
+    using C = Cfg<Tr, WM, WP, FM, FP, KVEC, (WEAVE >= 3 ? WEAVE - 1 : 0)>;
+    if constexpr (!(NHWC && WEAVE != 2 && sizeof(typename C::T) == 4)) {
+        return 0;
+    } else {
+        if (smax <= 0 || g.G > 1 || g.C % C::TK != 0) return 0;
+        const int nch = g.R * g.S * (g.C / C::TK);
+        const long long tiles = ((g.P_total + C::TP - 1) / C::TP) * (long long)((g.M + C::TM - 1) / C::TM);
+        const int S = sk_workgroups<Tr, WM, WP, FM, FP, WEAVE, KVEC, NHWC>(smax);
+        return S > 0 && use_stream_k(tiles, S, nch) ? S : 0;
+    }
 }
 
 template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE, bool KVEC, int EPI, bool NHWC, bool GRP = false>
 hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, int m_major,
-                      const void *zp, const Epi<EPI> &ep) {
+                      const void *zp, const Epi<EPI> &ep, const SkArgs &skin) {
     using C = Cfg<Tr, WM, WP, FM, FP, KVEC, (WEAVE >= 3 ? WEAVE - 1 : 0)>;
     using T = typename C::T;
     static_assert(EPI == 0 || (size_t)WM * 3 * C::TP * sizeof(double) <= C::LDS_BYTES, "epilogue fold fits LDS");
@@ -1111,7 +1321,14 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     const long long tiles_p = (g.P_total + C::TP - 1) / C::TP;
     const long long total = tiles_p * tiles_m;
     Epi<EPI> e = ep;
-    long long grid = total;
+    SkArgs sk{nullptr, nullptr, 0, 0};
+    if constexpr (NHWC && !GRP && WEAVE != 2) {
+        if (skin.S > 0 && skin.part && skin.cnt) {
+            const int S = sk_decide<Tr, WM, WP, FM, FP, WEAVE, KVEC, NHWC>(g, skin.S);
+            if (S > 0) sk = SkArgs{skin.part, skin.cnt, S, g.R * g.S * (g.C / C::TK)};
+        }
+    }
+    long long grid = sk.S > 0 ? sk.S : total;
     if constexpr (EPI != 0) {
         if (e.aux_kind == 1) {
             e.enc_vec = g.CHW % kEncVec == 0 && reinterpret_cast<uintptr_t>(D) % (kEncVec * sizeof(T)) == 0;
@@ -1127,7 +1344,7 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
             // first tiles run (spreading them through the grid measured slower: late ones stretch
             // the launch, interleaved ones slow the tiles beside them)
             e.aux_groups = (e.aux_blocks + 7) / 8;
-            grid = 8 * (e.aux_groups + (total + 7) / 8);
+            grid = 8 * (e.aux_groups + (grid + 7) / 8);
         } else {
             e.aux_groups = 0;
         }
@@ -1139,6 +1356,17 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
             reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS_BYTES);
         if (attr != hipSuccess) return attr;
     }
+    if constexpr (NHWC && !GRP && WEAVE != 2) {
+        if (sk.S > 0) {
+            kern = conv_kernel<Tr, WM, WP, FM, FP, WEAVE, KVEC, EPI, NHWC, GRP, true>;
+            if constexpr (C::LDS_BYTES > 65536) {
+                static const hipError_t attr_sk = hipFuncSetAttribute(
+                    reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                    (int)C::LDS_BYTES);
+                if (attr_sk != hipSuccess) return attr_sk;
+            }
+        }
+    }
     KernelEvents &ev = kernel_events();
     if (ev.before) {
         const hipError_t r = hipEventRecord(ev.before, st);
@@ -1146,7 +1374,7 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     }
     kern<<<(unsigned)grid, C::NT, C::LDS_BYTES, st>>>(static_cast<const T *>(D),
                                                                static_cast<const T *>(W), static_cast<T *>(O), g,
-                                                               tiles_m, (int)total, m_major, zp, e);
+                                                               tiles_m, (int)total, m_major, zp, e, sk);
     const hipError_t r = hipGetLastError();
     if (r != hipSuccess) return r;
     if (ev.after) {
@@ -1165,25 +1393,33 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     static constexpr int WEAVE_KIND = WEAVE;
     static constexpr int NT = Cfg<Tr, WM, WP, FM, FP>::NT;
     static constexpr size_t LDS_BYTES = Cfg<Tr, WM, WP, FM, FP, true, (WEAVE >= 3 ? WEAVE - 1 : 0)>::LDS_BYTES;
+    // stream-K workgroups of the channels-last form on the current device (0: whole tiles)
+    static int stream_k(const Geom &g, int smax) {
+        if constexpr (WEAVE == 2) return 0;
+        else return sk_decide<Tr, WM, WP, FM, FP, WEAVE, true, true>(g, smax);
+    }
+    static constexpr bool SK_FORM = WEAVE != 2 && sizeof(typename Tr::T) == 4;
     // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
     template <int EPI>
     static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep,
-                          bool nhwc = false, const void *zp = nullptr) {
+                          bool nhwc = false, const void *zp = nullptr, const SkArgs &sk = SkArgs{nullptr, nullptr, 0, 0}) {
+        const SkArgs none{nullptr, nullptr, 0, 0};
         if constexpr (WEAVE >= 3) {
             // direct-to-LDS tiles exist for channels-last operands only, with the copy of D right
             // behind the zero page (one buffer descriptor reaches both)
             if (!nhwc || !zp || static_cast<const char *>(zp) + 256 != static_cast<const char *>(D))
                 return hipErrorInvalidValue;
-            return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
+            return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep, sk);
         } else {
             if constexpr (WEAVE != 2) {
                 if (nhwc && g.G > 1)   // grouped: the loop that skips other groups' channels
-                    return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true, true>(g, D, W, O, st, 0, zp, ep);
+                    return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true, true>(g, D, W, O, st, 0, zp, ep,
+                                                                                        none);
             }
-            if (nhwc) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep);
+            if (nhwc) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, true>(g, D, W, O, st, 0, zp, ep, sk);
             const bool kvec = g.K % Tr::VEC == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
-            if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, false>(g, D, W, O, st, 0, zp, ep);
-            return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI, false>(g, D, W, O, st, 0, zp, ep);
+            if (kvec) return launch_one<Tr, WM, WP, FM, FP, WEAVE, true, EPI, false>(g, D, W, O, st, 0, zp, ep, none);
+            return launch_one<Tr, WM, WP, FM, FP, WEAVE, false, EPI, false>(g, D, W, O, st, 0, zp, ep, none);
         }
     }
 };
@@ -1283,12 +1519,44 @@ hipError_t launch_conv(const Plan &pl, const void *D, const void *W, void *O, hi
     return with_tile(pl.g, false, [&](auto t) { return decltype(t)::run(pl.g, D, W, O, st, ep); });
 }
 
+void conv_sk_space(const Geom &g, bool nhwc, int *smax, size_t *part_bytes, long long *counters) {
+    *smax = 0;
+    *part_bytes = 0;
+    *counters = 0;
+    if (!nhwc || g.G > 1) return;
+    with_tile(g, true, [&](auto t) {
+        using Tt = decltype(t);
+        if constexpr (Tt::SK_FORM) {
+            // room for every workgroup the LDS of kSkComputeUnits compute units could hold
+            const int waves = Tt::NT / 64;
+            long long per_cu = 160LL * 1024 / (long long)Tt::LDS_BYTES;
+            per_cu = per_cu < 32 / waves ? per_cu : 32 / waves;
+            *smax = (int)(per_cu * kSkComputeUnits / 8 * 8);
+            *part_bytes = (size_t)*smax * 2 * Tt::TM * Tt::TP * sizeof(float);
+            *counters = n_tiles(g, Tt::TM, Tt::TP);
+        }
+        return 0;
+    });
+}
+
+int conv_stream_k(const Plan &pl) {
+    if (!pl.nhwc || pl.sk_smax <= 0) return 0;
+    return with_tile(pl.g, true, [&](auto t) { return decltype(t)::stream_k(pl.g, pl.sk_smax); });
+}
+
 void conv_tile_shape(const Geom &g, bool nhwc, int *threads, size_t *lds_bytes) {
     with_tile(g, nhwc, [&](auto t) {
         *threads = decltype(t)::NT;
         *lds_bytes = decltype(t)::LDS_BYTES;
         return 0;
     });
+}
+
+// The stream-K scratch of the plan (none when the plan has no room for it).
+SkArgs sk_args(const Plan &pl, void *ws) {
+    if (pl.sk_smax <= 0) return SkArgs{nullptr, nullptr, 0, 0};
+    char *w = static_cast<char *>(ws);
+    return SkArgs{reinterpret_cast<float *>(w + pl.off_skpart), reinterpret_cast<int *>(w + pl.off_skcnt), pl.sk_smax, 0};
 }
 
 hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
@@ -1331,12 +1599,14 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
     const float *bias = ck ? ck->bias : nullptr;
     if (nf == 0) {
         Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
-        return with_tile(pl.g, pl.nhwc, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp); });
+        return with_tile(pl.g, pl.nhwc,
+                         [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp, sk_args(pl, ws)); });
     }
     Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
-    return with_tile(pl.g, pl.nhwc, [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp); });
+    return with_tile(pl.g, pl.nhwc,
+                     [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp, sk_args(pl, ws)); });
 }
 
 hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O, void *ws, hipStream_t st,
@@ -1347,7 +1617,7 @@ hipError_t launch_conv_ws(const Plan &pl, const void *D, const void *W, void *O,
     char *w = static_cast<char *>(ws);
     const Epi<0> ep{bias};
     return with_tile(pl.g, true, [&](auto t) {
-        return decltype(t)::run(pl.g, w + pl.off_dt, w + pl.off_wt, O, st, ep, true, w + pl.off_zero);
+        return decltype(t)::run(pl.g, w + pl.off_dt, w + pl.off_wt, O, st, ep, true, w + pl.off_zero, sk_args(pl, ws));
     });
 }
 

@@ -62,6 +62,9 @@ struct Plan {
     CocTile co;                       // their tiling (co_in_conv)
     size_t off_flags, off_enc, off_ver, off_sums, off_corr, off_dt, off_wt, off_encp, off_copart, off_zero,
         off_wchk, off_wfull, bytes;
+    int sk_smax;                      // stream-K workgroups the scratch has room for (0: none)
+    size_t off_skpart, off_skcnt;     // their partial accumulators, and one arrival count per tile
+    long long sk_counters;
     size_t corr_stride;               // doubles of the decision stage's per-position arrays
 };
 
@@ -237,6 +240,15 @@ void conv_tile_info(const Geom &g, bool nhwc, int out[6]);
 int conv_tile_m(const Geom &g, bool nhwc);
 // Threads per workgroup and dynamic LDS bytes of the convolution chosen for this layer.
 void conv_tile_shape(const Geom &g, bool nhwc, int *threads, size_t *lds_bytes);
+// Stream-K scratch of a layer's channels-last convolution: at most smax workgroups, part_bytes of
+// partial accumulators, one int counter per tile (all zero when its kernel has no stream-K form).
+// Sized for kSkComputeUnits compute units; a device with more runs at most smax workgroups.
+constexpr int kSkComputeUnits = 256;
+void conv_sk_space(const Geom &g, bool nhwc, int *smax, size_t *part_bytes, long long *counters);
+// Stream-K workgroups the plan's channels-last convolution launches on the current device (0: one
+// workgroup per tile).
+struct Plan;
+int conv_stream_k(const Plan &pl);
 // Layers whose convolution reads channels-last copies (pl.nhwc): Ch a multiple of 32 (and
 // kernels of at most 4096 taps, whose weight rows the copy stages in LDS).
 inline bool nhwc_layer(const Geom &g) { return g.C % 32 == 0 && g.R * g.S <= 4096; }

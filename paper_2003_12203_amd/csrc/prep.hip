@@ -58,7 +58,8 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(const T *__restrict__ D,
                                                         T *__restrict__ Dt, T *__restrict__ Wt, Geom g,
                                                         double *cd1, double *cd2, long long split_stride,
                                                         int tr_blocks, int hw_tiles, int c_tiles, int ns, int vec_d,
-                                                        int vec_w, uint4 *__restrict__ zero16) {
+                                                        int vec_w, uint4 *__restrict__ zero16, int *__restrict__ skcnt,
+                                                        int skcnt_n) {
     using P = PrepT<T, TC, SHIFT>;
     constexpr int VEC = P::VEC, TH = P::TH, LDT = P::LDT, RPT = P::RPT, BATCH = P::BATCH;
     __shared__ T tile[BATCH][TC][LDT];
@@ -185,6 +186,8 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(const T *__restrict__ D,
     const int m = b - tr_blocks;
     if (m >= g.M) return;
     if (m == 0 && threadIdx.x < 16) zero16[threadIdx.x] = make_uint4(0, 0, 0, 0);
+    // the convolution's stream-K arrival counts, spread over the weight workgroups
+    for (int i = m * kThreads + threadIdx.x; i < skcnt_n; i += g.M * kThreads) skcnt[i] = 0;
     T *stage = &tile[0][0][0];
     const int RS = g.R * g.S;
     const T *wm = W + (long long)m * g.K;
@@ -244,6 +247,9 @@ hipError_t run_tc(const Plan &pl, const void *D, const void *W, double *cd1, dou
     T *Dt = reinterpret_cast<T *>(w + pl.off_dt);
     T *Wt = reinterpret_cast<T *>(w + pl.off_wt);
     uint4 *zero16 = reinterpret_cast<uint4 *>(w + pl.off_zero);
+    int *skcnt = reinterpret_cast<int *>(w + pl.off_skcnt);
+    if (pl.sk_counters > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    const int skcnt_n = (int)pl.sk_counters;
     const long long HW = (long long)g.H * g.W;
     const long long hw_tiles = (HW + P::TH - 1) / P::TH, c_tiles = g.C / TC;
     // without the encode every round of images is a workgroup of its own
@@ -265,11 +271,11 @@ hipError_t run_tc(const Plan &pl, const void *D, const void *W, double *cd1, dou
     if (cd1)
         prep_kernel<T, true, TC, SHIFT><<<(unsigned)grid, kThreads, 0, st>>>(
             static_cast<const T *>(D), static_cast<const T *>(W), Dt, Wt, g, o1, o2, stride, (int)tr, (int)hw_tiles,
-            (int)c_tiles, ns, vec_d, vec_w, zero16);
+            (int)c_tiles, ns, vec_d, vec_w, zero16, skcnt, skcnt_n);
     else
         prep_kernel<T, false, TC, SHIFT><<<(unsigned)grid, kThreads, 0, st>>>(
             static_cast<const T *>(D), static_cast<const T *>(W), Dt, Wt, g, nullptr, nullptr, 0, (int)tr,
-            (int)hw_tiles, (int)c_tiles, ns, vec_d, vec_w, zero16);
+            (int)hw_tiles, (int)c_tiles, ns, vec_d, vec_w, zero16, skcnt, skcnt_n);
     return hipGetLastError();
 }
 
