@@ -828,8 +828,9 @@ def _short(name):
 def _conv_args(short):
     """(TM, TP, TK, loop, EPI, NHWC, GRP) of a conv_kernel instantiation name, else None."""
     import re
+    # the last argument, when present, marks the stream-K form of the same tile
     m = re.match(r"conv_kernel<(F32T|BF16T)<(\d+)>, (\d+), (\d+), (\d+), (\d+), (\d+|true|false), "
-                 r"(true|false), (\d), (true|false), (true|false)>", short)
+                 r"(true|false), (\d), (true|false), (true|false)(?:, (?:true|false))?>", short)
     if not m:
         return None
     tk = int(m.group(2))

@@ -626,18 +626,21 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
 //               channels-last copy, and compute the Co5..Co7 partial products
 //               (coc_tile.h).
 struct NoFaults {};
-// Stream-K schedule of the channels-last and direct-to-LDS loops (S > 0): the launch has S
-// workgroups (after the extra ones), and workgroup w runs the iterations [w U / S, (w + 1) U / S)
-// of the U = tiles x nch (tile, chunk) pairs in tile order, so every workgroup gets the same
-// share of matrix work whatever the tile count.  A tile whose chunks span several workgroups is
-// summed by the last of them to arrive: each writes its partial accumulators to a slot (0: the
-// workgroup's first segment, 1: its last), counts itself in cnt[tile], and the last adds the
-// slots in chunk order (a fixed order, whichever workgroup is last) before the epilogue.
+// Stream-K schedule of the channels-last loops (S > 0): the launch has S workgroups (after the
+// extra ones), as many as are resident at once.  The first dp_waves x S tiles run whole, tile
+// r S + w being workgroup w's r-th, so that the workgroups resident together work on neighbouring
+// tiles, as in the plain grid.  The last one to two waves' tiles (T of them) are shared evenly:
+// workgroup w runs their iterations [w U / S, (w + 1) U / S) of the U = T x nch (tile, chunk)
+// pairs in tile order.  A tile whose chunks span several workgroups is summed by the last of them
+// to arrive: each writes its partial accumulators to a slot (0: the workgroup's first shared
+// segment, 1: its last), counts itself in cnt[tile], and the last adds the slots in chunk order (a
+// fixed order, whichever workgroup is last) before the epilogue.
 struct SkArgs {
-    float *part;   // [S][2][TM * TP]
-    int *cnt;      // [tiles], zero at the launch (the channels-last copy clears it); left zero
-    int S;         // 0: one tile per workgroup
-    int nch;       // chunks per tile
+    float *part;    // [S][2][TM * TP]
+    int *cnt;       // [tiles], zero at the launch (the channels-last copy clears it); left zero
+    int S;          // 0: one tile per workgroup
+    int nch;        // chunks per tile
+    int dp_waves;   // waves of whole tiles before the shared ones
 };
 template <int EPI> struct Epi {
     double *part;
@@ -713,19 +716,21 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     // loops that can run a range of a tile's chunks (channels-last, dense)
     constexpr bool SKOK = SK && NHWC && !GRP && WEAVE != 2;
     constexpr bool skm = SKOK;
-    long long sk_it = 0, sk_end = 0, sk_u = 0;
-    int wl = 0;
+    long long sk_it = 0, sk_end = 0, sk_u = 0, sk_i0 = 0;
+    int wl = 0, dp = 0;
     if (skm) {
         if (bid >= sk.S) return;
-        // contiguous iteration ranges per XCD, as the tile order below
+        // contiguous tiles and iteration ranges per XCD, as the tile order below
         wl = xcd_tile(bid, sk.S);
-        sk_u = (long long)tiles_total * sk.nch;
-        sk_it = (long long)wl * sk_u / sk.S;
-        sk_end = (long long)(wl + 1) * sk_u / sk.S;
+        sk_i0 = (long long)sk.dp_waves * sk.S * sk.nch;   // the first shared iteration
+        sk_u = (long long)tiles_total * sk.nch - sk_i0;
+        sk_it = sk_i0 + (long long)wl * sk_u / sk.S;
+        sk_end = sk_i0 + (long long)(wl + 1) * sk_u / sk.S;
     } else if (bid >= tiles_total) {
         return;
     }
-    bool first_seg = true;
+    bool first_seg = true;    // the next shared segment is this workgroup's first
+    bool first_iter = true;
     const Geom &g_all = g;
     for (;;) {
     // In the stream-K kernel the thread index and the geometry are passed through empty asm at
@@ -746,11 +751,16 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
     // the segment: chunks [k0, k0 + kn) of one tile (kn < 0: the whole tile)
     int tile, k0 = 0, kn = -1;
     if (skm) {
-        if (sk_it >= sk_end) break;
-        tile = (int)(sk_it / sk.nch);
-        k0 = (int)(sk_it - (long long)tile * sk.nch);
-        kn = (int)(sk_end - sk_it < (long long)(sk.nch - k0) ? sk_end - sk_it : (long long)(sk.nch - k0));
-        if (!first_seg) __syncthreads();   // every wave is done with the last segment's LDS
+        if (dp < sk.dp_waves) {
+            tile = dp * sk.S + wl;
+            kn = sk.nch;
+        } else {
+            if (sk_it >= sk_end) break;
+            tile = (int)(sk_it / sk.nch);
+            k0 = (int)(sk_it - (long long)tile * sk.nch);
+            kn = (int)(sk_end - sk_it < (long long)(sk.nch - k0) ? sk_end - sk_it : (long long)(sk.nch - k0));
+        }
+        if (!first_iter) __syncthreads();   // every wave is done with the last segment's LDS
     } else {
         // logical tile order: pixel-major keeps the M tiles of one pixel tile on one
         // XCD (its L2 serves the repeated D reads); M-major keeps one slab of W
@@ -963,7 +973,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             // a part of the tile: publish it; the last of the tile's workgroups sums them all
             const long long ib = (long long)tile * sk.nch;
             // the workgroup whose range holds iteration i
-            auto owner = [&](long long i) { return (int)(((i + 1) * sk.S - 1) / sk_u); };
+            auto owner = [&](long long i) { return (int)(((i - sk_i0 + 1) * sk.S - 1) / sk_u); };
             const int w0 = owner(ib), w1 = owner(ib + sk.nch - 1);
             constexpr int NR = FM * FP * 16;   // accumulators per thread; slot layout [NR][NT]
             float *mine = sk.part + ((size_t)wl * 2 + (first_seg ? 0 : 1)) * (size_t)(C::TM * C::TP);
@@ -992,6 +1002,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             if (!last) {
                 sk_it += kn;
                 first_seg = false;
+                first_iter = false;
                 continue;
             }
             // the other parts, read with device-coherent loads after the count said they are all there
@@ -1002,7 +1013,7 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             // the accumulators.
             static_assert(NR * C::NT == C::TM * C::TP, "slot size");
             for (int w = w0; w <= w1; ++w) {
-                const int slot = (long long)w * sk_u / sk.S >= ib ? 0 : 1;
+                const int slot = sk_i0 + (long long)w * sk_u / sk.S >= ib ? 0 : 1;
                 const float *src = sk.part + ((size_t)w * 2 + slot) * (size_t)(C::TM * C::TP) + tid;
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
@@ -1229,8 +1240,13 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
         }
     }
     if (!skm) break;
-    sk_it += kn;
-    first_seg = false;
+    first_iter = false;
+    if (dp < sk.dp_waves) {
+        ++dp;
+    } else {
+        sk_it += kn;
+        first_seg = false;
+    }
     }   // segments
 }
 
@@ -1321,11 +1337,15 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
     const long long tiles_p = (g.P_total + C::TP - 1) / C::TP;
     const long long total = tiles_p * tiles_m;
     Epi<EPI> e = ep;
-    SkArgs sk{nullptr, nullptr, 0, 0};
+    SkArgs sk{nullptr, nullptr, 0, 0, 0};
     if constexpr (NHWC && !GRP && WEAVE != 2) {
         if (skin.S > 0 && skin.part && skin.cnt) {
             const int S = sk_decide<Tr, WM, WP, FM, FP, WEAVE, KVEC, NHWC>(g, skin.S);
-            if (S > 0) sk = SkArgs{skin.part, skin.cnt, S, g.R * g.S * (g.C / C::TK)};
+            if (S > 0) {
+                // whole-tile waves but for the last one to two, whose tiles are shared
+                const long long waves = (total + S - 1) / S;
+                sk = SkArgs{skin.part, skin.cnt, S, g.R * g.S * (g.C / C::TK), (int)(waves > 2 ? waves - 2 : 0)};
+            }
         }
     }
     long long grid = sk.S > 0 ? sk.S : total;
@@ -1402,7 +1422,7 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
     // NCHW: D and W as given; NHWC: the channels-last copies Dt and Wt (always aligned, K % VEC == 0)
     template <int EPI>
     static hipError_t run(const Geom &g, const void *D, const void *W, void *O, hipStream_t st, const Epi<EPI> &ep,
-                          bool nhwc = false, const void *zp = nullptr, const SkArgs &sk = SkArgs{nullptr, nullptr, 0, 0}) {
+                          bool nhwc = false, const void *zp = nullptr, const SkArgs &sk = SkArgs{nullptr, nullptr, 0, 0, 0}) {
         const SkArgs none{nullptr, nullptr, 0, 0};
         if constexpr (WEAVE >= 3) {
             // direct-to-LDS tiles exist for channels-last operands only, with the copy of D right
@@ -1463,6 +1483,18 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
         // grouped layers: rows of tiles inside one group, so that every tile skips the other
         // groups' channels (192 filters a group: 64-row tiles)
         if (g.G > 1 && g.Mg % 128 != 0 && g.Mg % 64 == 0) return f(F32_64x64{});
+        // dense channels-last layers whose tiles the stream-K schedule shares out evenly (at the two
+        // workgroups a compute unit that these tiles keep on 256 compute units) lose nothing to the
+        // last round of tiles: there the larger tile is the faster one per output (VGG-19 v5-v9:
+        // 128 x 128 3-5 % faster than 128 x 64; v13-v16, Darknet-19 c9-c18 and AlexNet conv5:
+        // 128 x 64 6-9 % faster than 64 x 64 or 128 x 128)
+        if (nhwc && g.G == 1) {
+            auto shared = [&](long long tiles, int tk) {
+                return g.C % tk == 0 && use_stream_k(tiles, 2 * kSkComputeUnits, g.R * g.S * (g.C / tk));
+            };
+            if (n_tiles(g, 128, 128) >= 600 && shared(n_tiles(g, 128, 128), 16)) return f(F32_128x128{});
+            if (n_tiles(g, 128, 64) >= 256 && shared(n_tiles(g, 128, 64), 32)) return f(F32_128x64{});
+        }
         // the tile with the least predicted time: the padded outputs (tiles x TM x TP), plus half of
         // the idle slots in the last round of 256 tiles, at the tile's own rate per output
         // (128 x 128 : 128 x 64 : 64 x 64 = 1 : 0.972 : 0.925).  The one-half and the rates are
@@ -1554,9 +1586,10 @@ void conv_tile_shape(const Geom &g, bool nhwc, int *threads, size_t *lds_bytes) 
 
 // The stream-K scratch of the plan (none when the plan has no room for it).
 SkArgs sk_args(const Plan &pl, void *ws) {
-    if (pl.sk_smax <= 0) return SkArgs{nullptr, nullptr, 0, 0};
+    if (pl.sk_smax <= 0) return SkArgs{nullptr, nullptr, 0, 0, 0};
     char *w = static_cast<char *>(ws);
-    return SkArgs{reinterpret_cast<float *>(w + pl.off_skpart), reinterpret_cast<int *>(w + pl.off_skcnt), pl.sk_smax, 0};
+    return SkArgs{reinterpret_cast<float *>(w + pl.off_skpart), reinterpret_cast<int *>(w + pl.off_skcnt), pl.sk_smax, 0,
+                  0};
 }
 
 hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *O, const ftcnn_checksums *ck,
