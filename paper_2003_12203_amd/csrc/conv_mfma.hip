@@ -1459,6 +1459,7 @@ long long n_tiles(const Geom &g, int tm, int tp) {
 
 using F32_M32 = Tile<F32T<16>, 1, 4, 1, 2, true>;
 using F32_M64 = Tile<F32T<16>, 2, 2, 1, 2, true>;
+using F32_64x256 = Tile<F32T<16>, 1, 4, 2, 2, true>;   // channels-last M <= 64: 64 x 64 a wave
 using F32_M96 = Tile<F32T<16>, 1, 4, 3, 1, true>;   // 96 x 128: AlexNet conv1 gets 1513 tiles, 3 full rounds
 using F32_128x128 = Tile<F32T<16>, 2, 2, 2, 2, true>;
 using F32_128x64 = Tile<F32T<32>, 2, 2, 2, 1, true>;
@@ -1478,7 +1479,9 @@ template <typename Fn>
 auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
     if (g.dtype == FTCNN_F32) {
         if (g.M <= 32) return f(F32_M32{});
-        if (g.M <= 64) return f(F32_M64{});
+        // on channels-last layers a wave of the 64 x 256 tile holds 64 x 64 outputs, as in the
+        // 128 x 128 tile (VGG-19 v2 1309 -> 1284 us, Darknet-19 c2 349 -> 334 us protected)
+        if (g.M <= 64) return nhwc ? f(F32_64x256{}) : f(F32_M64{});
         if (g.M <= 96) return f(F32_M96{});
         // grouped layers: rows of tiles inside one group, so that every tile skips the other
         // groups' channels (192 filters a group: 64-row tiles)

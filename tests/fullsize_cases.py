@@ -15,7 +15,7 @@ CASES = [
     ("darknet19", "c1", 1, False, 1),     # fp32 32 x 256, gathered from NCHW (3-channel stem)
     ("alexnet", "conv1", 1, False, 1),    # fp32 96 x 128, NCHW, 11x11 stride 4
     ("vgg19", "v1", 1, False, 1),         # fp32 64 x 128, NCHW
-    ("darknet19", "c4", 1, False, 1),     # fp32 64 x 128, channels-last, 1x1
+    ("darknet19", "c4", 1, False, 1),     # fp32 64 x 256, channels-last, 1x1
     ("alexnet", "conv5", 1, False, 1),    # fp32 128 x 64, channels-last, stream-K
     ("darknet19", "c10", 1, False, 1),    # fp32 64 x 64, channels-last, 1x1
     ("alexnet", "conv4", 1, False, 1),    # fp32 128 x 64, channels-last
