@@ -1462,6 +1462,7 @@ using F32_M64 = Tile<F32T<16>, 2, 2, 1, 2, true>;
 using F32_64x256 = Tile<F32T<16>, 1, 4, 2, 2, true>;   // channels-last M <= 64: 64 x 64 a wave
 using F32_M96 = Tile<F32T<16>, 1, 4, 3, 1, true>;   // 96 x 128: AlexNet conv1 gets 1513 tiles, 3 full rounds
 using F32_128x128 = Tile<F32T<16>, 2, 2, 2, 2, true>;
+using F32_128x128_K32 = Tile<F32T<32>, 2, 2, 2, 2, true>;   // 32-deep chunks: half the barriers
 using F32_128x64 = Tile<F32T<32>, 2, 2, 2, 1, true>;
 using F32_64x64 = Tile<F32T<32>, 2, 2, 1, 1, true>;
 using BF16_M32 = Tile<BF16T<32>, 1, 4, 1, 2, 0>;
@@ -1495,7 +1496,10 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
             auto shared = [&](long long tiles, int tk) {
                 return g.C % tk == 0 && use_stream_k(tiles, 2 * kSkComputeUnits, g.R * g.S * (g.C / tk));
             };
-            if (n_tiles(g, 128, 128) >= 600 && shared(n_tiles(g, 128, 128), 16)) return f(F32_128x128{});
+            // with 512 or more channels the 32-deep chunks pay (VGG-19 v10-v12 1013 -> 986 us; on
+            // v3-v8, 64 to 256 channels, they were up to 2.6 % slower)
+            if (n_tiles(g, 128, 128) >= 600 && shared(n_tiles(g, 128, 128), 16))
+                return g.C >= 512 ? f(F32_128x128_K32{}) : f(F32_128x128{});
             if (n_tiles(g, 128, 64) >= 256 && shared(n_tiles(g, 128, 64), 32)) return f(F32_128x64{});
         }
         // the tile with the least predicted time: the padded outputs (tiles x TM x TP), plus half of

@@ -23,7 +23,7 @@ CASES = [
     ("alexnet", "conv2", 1, True, 1),     # ... with a bias in the epilogue (Sec. 5.1)
     ("alexnet", "conv2", 2, False, 1),    # fp32 128 x 128, channels-last, grouped channel skip (Sec. 5.2)
     ("alexnet", "conv4", 2, False, 1),    # fp32 64 x 64, channels-last, grouped channel skip
-    ("vgg19", "v10", 1, True, 1),         # fp32 128 x 128 with a bias, 512 channels, stream-K
+    ("vgg19", "v10", 1, True, 1),         # fp32 128 x 128, 32-deep chunks, with a bias, stream-K
     ("vgg19_bf16", "v1", 1, False, 1),    # bf16 64 x 256, NCHW
     ("resnet18", "l1.0", 1, False, 1),    # bf16 64 x 256, channels-last, two chunks in flight
     ("resnet18", "l3.0", 1, False, 1),    # bf16 128 x 128, direct-to-LDS
