@@ -618,13 +618,15 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
 // rows give sum O, sum (m + wbase) O, (n + wbase) sum O and sum O^2, written as
 // slice (tile_m * N + n) of a [slices][4][E*F] float64 array; block 0 resets the
 // report.  EPI 2: EPI 1 with faults planted in the stored values first.
-// With EPI 1 and 2 the first aux_groups groups of eight consecutive workgroup
-// ids (one per XCD) may do other work of the protected layer instead of a tile,
-// memory-bound work that runs beside the matrix-bound tiles of the same launch:
-//   aux_kind 1: encode the input checksums Cd1, Cd2 of D (Sec. 3.2);
+// With EPI 1 and 2, aux_groups groups of eight consecutive workgroup ids (one per
+// XCD) may do other work of the protected layer instead of a tile, memory-bound work
+// that runs beside the matrix-bound tiles of the same launch:
+//   aux_kind 1: encode the input checksums Cd1, Cd2 of D (Sec. 3.2), in the first
+//               groups of the grid (they read D as the first tiles do);
 //   aux_kind 2: combine the image-split partials of Cd1, Cd2 left by the
 //               channels-last copy, and compute the Co5..Co7 partial products
-//               (coc_tile.h).
+//               (coc_tile.h), in the last groups, after the tile_groups groups of
+//               tiles, where they fill the slots the tiles' last round leaves.
 struct NoFaults {};
 // Stream-K schedule of the channels-last loops (S > 0): the launch has S workgroups (after the
 // extra ones), as many as are resident at once.  The first dp_waves x S tiles run whole, tile
@@ -647,6 +649,7 @@ template <int EPI> struct Epi {
     ftcnn_report *rep;
     int cap;
     int aux_kind, aux_blocks, aux_groups;
+    int tile_groups;     // groups of eight tile workgroups in front of the aux_kind 2 ones
     double *cd1, *cd2;   // kind 1: encoded here; kind 2: written by the combine workgroups
     int enc_vec;         // kind 1: 16-byte loads
     CdSrc src;           // kind 2
@@ -694,7 +697,16 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
             ep.rep->reserved[1] = ep.co_slices;
         }
         if (ep.aux_groups > 0) {
-            if ((bid >> 3) < ep.aux_groups) {
+            int ab = -1;   // this workgroup's index among the extra ones
+            if (ep.aux_kind == 2) {
+                if ((bid >> 3) >= ep.tile_groups) ab = bid - 8 * ep.tile_groups;
+            } else if ((bid >> 3) < ep.aux_groups) {
+                ab = bid;
+            } else {
+                bid -= 8 * ep.aux_groups;   // keeps bid % 8, hence the XCD the tile order assumes
+            }
+            if (ab >= 0) {
+                const int bid = ab;
                 if (bid < ep.aux_blocks) {
                     if (ep.aux_kind == 1) {
                         if (ep.enc_vec) encode_block<T, C::NT, kEncVec>(D, g, bid, ep.cd1, ep.cd2);
@@ -708,7 +720,6 @@ __global__ __launch_bounds__(64 * WM * WP) void conv_kernel(const typename Tr::T
                 }
                 return;
             }
-            bid -= 8 * ep.aux_groups;   // keeps bid % 8, hence the XCD the tile order assumes
         }
     }
     constexpr bool DMA = NHWC && WEAVE >= 3 && sizeof(T) == 2 && C::TK == 64;
@@ -1360,10 +1371,11 @@ hipError_t launch_one(const Geom &g, const void *D, const void *W, void *O, hipS
         if (e.aux_kind == 2 && e.co_slices > 0 && (size_t)e.co.cc * coc_channel_bytes(g, e.co.ty, e.co.tx) > C::LDS_BYTES)
             return hipErrorInvalidValue;   // the plan sized the CoC window for this tile's LDS
         if (e.aux_kind != 0 && e.aux_blocks > 0) {
-            // all extra workgroups first: they start on every CU at once and are done while the
-            // first tiles run (spreading them through the grid measured slower: late ones stretch
-            // the launch, interleaved ones slow the tiles beside them)
+            // the encode first (it reads D beside the first tiles); the Co5..Co7 work after the
+            // tiles, in the slots their last round leaves (in front of them it held back the first
+            // tiles: VGG-19 bf16 v6 197 -> 190 us, VGG-19 fp32 overhead 4.4 -> 3.2 %)
             e.aux_groups = (e.aux_blocks + 7) / 8;
+            e.tile_groups = (int)((grid + 7) / 8);
             grid = 8 * (e.aux_groups + (grid + 7) / 8);
         } else {
             e.aux_groups = 0;
@@ -1638,11 +1650,11 @@ hipError_t launch_conv_sums(const Plan &pl, const void *D, const void *W, void *
     const double *cw1 = ck ? ck->cw1 : nullptr, *cw2 = ck ? ck->cw2 : nullptr;
     const float *bias = ck ? ck->bias : nullptr;
     if (nf == 0) {
-        Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
+        Epi<1> ep{part, rep, cap, aux_kind, aux_blocks, 0, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
         return with_tile(pl.g, pl.nhwc,
                          [&](auto t) { return decltype(t)::run(pl.g, Dc, Wc, O, st, ep, pl.nhwc, zp, sk_args(pl, ws)); });
     }
-    Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
+    Epi<2> ep{part, rep, cap, aux_kind, aux_blocks, 0, 0, cd1, cd2, 0, src, cw1, cw2, copart, co, co_slices, {}, bias};
     for (int i = 0; i < nf; ++i) ep.fl.f[i] = faults[i];
     ep.fl.n = nf;
     return with_tile(pl.g, pl.nhwc,
