@@ -566,19 +566,16 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
         // 32-bit wrap-around arithmetic: the sum with a valid tap's offset is the element's offset
         b_off[j] = 256u + 2u * (unsigned)(n * (int)g.CHW + (b_ih[j] * g.W + b_iw[j]) * g.C + cg * 8);
     }
-    // part q (of 4) of a chunk's loads: a quarter of the weight and of the input slots
-    static_assert(NIA % 4 == 0 && NIB % 4 == 0, "DMA slots split over the four k-steps");
+    // part q (of 4) of a chunk's loads: every fourth weight and input slot
     auto issue_part = [&](const TapWalk &t, unsigned char *base, int q) {
         const unsigned soff_a = 2u * (unsigned)t.kb(g);
         const unsigned tap = 2u * (unsigned)((t.r * g.W + t.s) * g.C + t.c0);
 #pragma unroll
-        for (int jj = 0; jj < NIA / 4; ++jj) {
-            const int j = q * (NIA / 4) + jj;
+        for (int j = q; j < NIA; j += 4) {
             buffer_load_lds16(rw, base + (j * NW + w) * 8 * 128, a_off[j], soff_a);
         }
 #pragma unroll
-        for (int jj = 0; jj < NIB / 4; ++jj) {
-            const int j = q * (NIB / 4) + jj;
+        for (int j = q; j < NIB; j += 4) {
             const bool ok = ((unsigned)(b_ih[j] + t.r) < (unsigned)g.H) & ((unsigned)(b_iw[j] + t.s) < (unsigned)g.W);
             buffer_load_lds16(rd, base + STAGE_A + (j * NW + w) * 8 * 128, ok ? b_off[j] + tap : 0u, 0u);
         }
@@ -1459,12 +1456,12 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
 // Tile choice per layer, from sweeps over the workload shapes on MI355X.  The
 // filter tile follows M so small-M layers waste no MFMA rows; for larger M the
 // biggest tile that still leaves about two workgroups per CU wins.  For bf16
-// (eight times the fp32 matrix rate per instruction) the channels-last loop
-// keeps two chunks in flight (WEAVE 2): 64 x 256 tiles for M <= 64, and for
-// 64-channel multiples direct-to-LDS loads (WEAVE 3): 256 x 256 tiles (eight
-// waves of 128 x 64) for M >= 256 where there are enough of them,
-// 128 x 128 elsewhere; other layers take 256 x 256 or 128 x 128 tiles with
-// register-staged loads.
+// (eight times the fp32 matrix rate per instruction), channels-last layers with
+// 64-channel multiples take direct-to-LDS loads (WEAVE 3): 64 x 256 tiles for
+// M <= 64, 256 x 256 tiles (eight waves of 128 x 64) for M >= 256 where there
+// are enough of them, 128 x 128 elsewhere; the other channels-last layers keep
+// two chunks in flight (WEAVE 2), and the rest take 64 x 256, 256 x 256 or
+// 128 x 128 tiles with register-staged loads.
 long long n_tiles(const Geom &g, int tm, int tp) {
     return ((g.P_total + tp - 1) / tp) * (long long)((g.M + tm - 1) / tm);
 }
@@ -1482,6 +1479,7 @@ using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, 2>;
 using BF16_128x128_K64 = Tile<BF16T<64>, 2, 2, 2, 2, 2>;
 using BF16_256x256 = Tile<BF16T<32>, 2, 2, 4, 4, 2>;
 using BF16_DMA_128x128 = Tile<BF16T<64>, 2, 2, 2, 2, 3>;
+using BF16_DMA_64x256 = Tile<BF16T<64>, 1, 4, 2, 2, 3>;   // M <= 64: four waves of 64 x 64
 // eight waves of 128 x 64 (two a SIMD, accumulators in 128 registers a lane): against four waves
 // of 128 x 128 (one a SIMD) 5-8 % faster on VGG-19 bf16 v5-v12, which also beat 128 x 128 tiles
 using BF16_DMA_256x256 = Tile<BF16T<64>, 2, 4, 4, 2, 3>;
@@ -1532,11 +1530,13 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
         if (c12864 <= c64) return f(F32_128x64{});
         return f(F32_64x64{});
     }
-    if (g.M <= 32) return f(BF16_M32{});
-    if (g.M <= 64) return f(BF16_M64{});
     // direct-to-LDS loads reach the operands through 32-bit buffer offsets
     const bool dma = nhwc && g.C % 64 == 0 && (long long)g.M * g.K * 2 < (1LL << 31) &&
                      256 + (long long)g.N * g.CHW * 2 < (1LL << 31);
+    if (g.M <= 32) return f(BF16_M32{});
+    // M <= 64 with 64-channel multiples: direct-to-LDS 64 x 256 (VGG-19 v2 384 -> 308 us, ResNet-18
+    // l1 109 -> 90 us for the convolution alone)
+    if (g.M <= 64) return dma ? f(BF16_DMA_64x256{}) : f(BF16_M64{});
     if (dma) {
         // 256 x 256 where M is large and there are enough such tiles
         if (g.M >= 256 && n_tiles(g, 256, 256) >= 192) return f(BF16_DMA_256x256{});
