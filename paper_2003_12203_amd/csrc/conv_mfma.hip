@@ -669,7 +669,7 @@ template <> struct Bits<float> {
 };
 template <> struct Bits<uint16_t> {
     using B = uint16_t;
-    __device__ static B make(float v) { return f32_to_bf16_bits(v); }
+    __device__ static B make(float v) { return f32_to_bf16_rne(v); }
     __device__ static float value(B b) { return bf16_bits_to_f32(b); }
 };
 

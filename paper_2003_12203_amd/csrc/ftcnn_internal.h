@@ -137,6 +137,10 @@ __host__ __device__ inline uint16_t f32_to_bf16_bits(float f) {
     return (uint16_t)(u >> 16);
 }
 
+// The same rounding (nearest, ties to even) in one gfx950 instruction (v_cvt_pk_bf16_f32),
+// for the output stores of the kernels; a NaN becomes a quiet NaN.
+__device__ inline uint16_t f32_to_bf16_rne(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
     __device__ static float load(const float *p, long long i) { return p[i]; }
@@ -144,7 +148,7 @@ template <> struct Elem<float> {
 };
 template <> struct Elem<uint16_t> {
     __device__ static float load(const uint16_t *p, long long i) { return bf16_bits_to_f32(p[i]); }
-    __device__ static void store(uint16_t *p, long long i, float v) { p[i] = f32_to_bf16_bits(v); }
+    __device__ static void store(uint16_t *p, long long i, float v) { p[i] = f32_to_bf16_rne(v); }
 };
 
 // ---- faults planted for testing (the paper's source-level injection, Sec. 6.1)
