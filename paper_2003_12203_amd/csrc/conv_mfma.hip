@@ -443,9 +443,13 @@ __device__ inline void chunk_f32(const float *As, const float *Bs, int lane, int
 // into LDS: lane L of a wave lands at the instruction's LDS base + 16*L (the
 // base is wave-uniform), while every lane picks its own global address.  The
 // tiles are kept as rows of 64 bf16 (128 bytes, eight 16-byte chunks) with
-// chunk c of row r stored at position c ^ (r & 7), so one instruction fills
-// eight whole rows and the matrix-core reads of 32 consecutive rows spread
-// over all banks.  Two LDS stages: chunk k + 2 is requested into the stage of
+// chunk c of row r stored at position c ^ ((r >> 1) & 7), so one instruction
+// fills eight whole rows, and a 16-byte fragment read of 16 consecutive rows
+// (what the LDS serves in one cycle: 256 bytes over 64 banks) touches 16
+// distinct 16-byte bank groups: rows 2i and 2i + 1 share a position but lie in
+// different halves of a 256-byte line.  (The row's own low bits, c ^ (r & 7),
+// put rows r and r + 8 on the same banks: two cycles a read, as the bank
+// conflict counter showed.)  Two LDS stages: chunk k + 2 is requested into the stage of
 // chunk k as soon as every wave has read chunk k, so a chunk's loads have a
 // whole chunk of MFMAs to land.  Waits on the loads are explicit (vmcnt), and
 // the barriers carry compiler-only fences: a memory fence would make the
@@ -474,7 +478,7 @@ __device__ inline void lds_barrier() {
 template <typename C, int FM, int FP>
 __device__ inline void mma_chunk_swz(const unsigned char *As, const unsigned char *Bs, int lane, int arow0, int brow0,
                                      floatx16 (&acc)[FM][FP]) {
-    const int l32 = lane & 31, h = lane >> 5, sw = l32 & 7;
+    const int l32 = lane & 31, h = lane >> 5, sw = (l32 >> 1) & 7;
     const unsigned char *arow = As + (arow0 + l32) * 128, *brow = Bs + (brow0 + l32) * 128;
     bf16x8 a[2][FM], b[2][FP];
     auto load = [&](int q, int slot) {
@@ -542,7 +546,9 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
     constexpr int STAGE_A = C::TM * 128, STAGE = (C::TM + C::TP) * 128;
     const int lane = tid & 63, w = tid >> 6;
     const int lr = lane >> 3;              // row of the instruction's eight
-    const int cg = (lane & 7) ^ lr;        // global chunk this lane loads (its LDS chunk is lane & 7)
+    // the global chunk this lane loads (its LDS chunk is lane & 7) for an instruction whose eight
+    // rows start at a multiple of 16 (sw = 0) or 8 mod 16 (sw = 4): row r's swizzle is (r >> 1) & 7
+    auto cg = [&](int sw) { return (lane & 7) ^ ((sw + (lr >> 1)) & 7); };
     const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(Wt, (int)((long long)g.M * g.K * 2));
     const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(zp_dt, (int)(256 + (long long)g.N * g.CHW * 2));
     unsigned a_off[NIA];
@@ -550,7 +556,7 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
     for (int j = 0; j < NIA; ++j) {
         int m = m0 + (j * NW + w) * 8 + lr;
         m = m < g.M ? m : g.M - 1;
-        a_off[j] = (unsigned)(m * g.K + cg * 8) * 2u;
+        a_off[j] = (unsigned)(m * g.K + cg(4 * ((j * NW + w) & 1)) * 8) * 2u;
     }
     unsigned b_off[NIB];
     int b_ih[NIB], b_iw[NIB];
@@ -564,7 +570,8 @@ __device__ inline void dma_mainloop(const uint16_t *__restrict__ Wt, const Geom 
         b_ih[j] = g.U * x - g.P;
         b_iw[j] = g.U * y - g.P;
         // 32-bit wrap-around arithmetic: the sum with a valid tap's offset is the element's offset
-        b_off[j] = 256u + 2u * (unsigned)(n * (int)g.CHW + (b_ih[j] * g.W + b_iw[j]) * g.C + cg * 8);
+        b_off[j] = 256u + 2u * (unsigned)(n * (int)g.CHW + (b_ih[j] * g.W + b_iw[j]) * g.C +
+                                          cg(4 * ((j * NW + w) & 1)) * 8);
     }
     // part q (of 4) of a chunk's loads: every fourth weight and input slot
     auto issue_part = [&](const TapWalk &t, unsigned char *base, int q) {
