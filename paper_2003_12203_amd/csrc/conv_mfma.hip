@@ -156,14 +156,28 @@ __device__ inline typename C::Mask load_b(const typename C::T *__restrict__ Dt, 
     const int HW = g.H * g.W;
     int koff = c * HW + r * g.W + s;
     const int wrap_s = g.W - g.S, wrap_r = HW - g.R * g.W;
+    // bf16: the loads go through a buffer descriptor of D, and an element outside the image, past K
+    // or of a pixel past the end takes an offset past the buffer, whose load returns zero: no
+    // validity bits and no 64-bit address per element (2 N C H W bytes < 2^32: make_plan keeps
+    // N C H W below 2^31)
+    [[maybe_unused]] __amdgpu_buffer_rsrc_t rd;
+    if constexpr (sizeof(T) == 2)
+        rd = __builtin_amdgcn_make_buffer_rsrc(const_cast<T *>(Dt), (short)0,
+                                               (int)(unsigned)(2ull * (unsigned long long)g.N * (unsigned long long)g.CHW),
+                                               0x00020000);
 #pragma unroll
     for (int j = 0; j < C::KR; ++j) {
         const int ih = ih0 + r, iw = iw0 + s;
         // bitwise, not short-circuit: no branches in the gather
         const bool ok = pvalid & (kstart + j < g.K) & ((unsigned)ih < (unsigned)g.H) &
                         ((unsigned)iw < (unsigned)g.W);
-        rb[j / C::VEC].e[j % C::VEC] = Dt[ok ? lane_base + koff : 0];
-        mask |= (ok ? M(1) : M(0)) << j;
+        if constexpr (sizeof(T) == 2) {
+            rb[j / C::VEC].e[j % C::VEC] =
+                __builtin_amdgcn_raw_buffer_load_b16(rd, ok ? 2u * (unsigned)(lane_base + koff) : 0xFFFFFFFEu, 0, 0);
+        } else {
+            rb[j / C::VEC].e[j % C::VEC] = Dt[ok ? lane_base + koff : 0];
+            mask |= (ok ? M(1) : M(0)) << j;
+        }
         // advance (c, r, s) by one k with selects (scalar registers)
         ++s;
         ++koff;
@@ -176,6 +190,7 @@ __device__ inline typename C::Mask load_b(const typename C::T *__restrict__ Dt, 
         koff += wr ? wrap_r : 0;
         c += wr ? 1 : 0;
     }
+    if constexpr (sizeof(T) == 2) return ~M(0);   // every invalid element is a zero already
     return mask;
 }
 
