@@ -1479,7 +1479,7 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
 // filter tile follows M so small-M layers waste no MFMA rows; for larger M the
 // biggest tile that still leaves about two workgroups per CU wins.  For bf16
 // (eight times the fp32 matrix rate per instruction), channels-last layers with
-// 64-channel multiples take direct-to-LDS loads (WEAVE 3): 64 x 256 tiles for
+// 64-channel multiples take direct-to-LDS loads (WEAVE 3): 64 x 128 tiles for
 // M <= 64, 256 x 256 tiles (eight waves of 128 x 64) for M >= 256 where there
 // are enough of them, 128 x 128 elsewhere; the other channels-last layers keep
 // two chunks in flight (WEAVE 2), and the rest take 64 x 256, 256 x 256 or
@@ -1501,7 +1501,11 @@ using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, 2>;
 using BF16_128x128_K64 = Tile<BF16T<64>, 2, 2, 2, 2, 2>;
 using BF16_256x256 = Tile<BF16T<32>, 2, 2, 4, 4, 2>;
 using BF16_DMA_128x128 = Tile<BF16T<64>, 2, 2, 2, 2, 3>;
-using BF16_DMA_64x256 = Tile<BF16T<64>, 1, 4, 2, 2, 3>;   // M <= 64: four waves of 64 x 64
+// M <= 64: four waves of 64 x 32, a 48 KB ring, three workgroups a compute unit (against 64 x 256
+// tiles of four 64 x 64 waves, two a compute unit: ResNet-18 l1 89 -> 79 us, VGG-19 v2 299 -> 287 us
+// with the channels-last copy; 64 x 64 tiles of two waves, 64 x 128 of two waves and deeper rings
+// were slower)
+using BF16_DMA_64x128 = Tile<BF16T<64>, 1, 4, 2, 1, 3>;
 // eight waves of 128 x 64 (two a SIMD, accumulators in 128 registers a lane): against four waves
 // of 128 x 128 (one a SIMD) 5-8 % faster on VGG-19 bf16 v5-v12, which also beat 128 x 128 tiles
 using BF16_DMA_256x256 = Tile<BF16T<64>, 2, 4, 4, 2, 3>;
@@ -1556,9 +1560,10 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
     const bool dma = nhwc && g.C % 64 == 0 && (long long)g.M * g.K * 2 < (1LL << 31) &&
                      256 + (long long)g.N * g.CHW * 2 < (1LL << 31);
     if (g.M <= 32) return f(BF16_M32{});
-    // M <= 64 with 64-channel multiples: direct-to-LDS 64 x 256 (VGG-19 v2 384 -> 308 us, ResNet-18
-    // l1 109 -> 90 us for the convolution alone)
-    if (g.M <= 64) return dma ? f(BF16_DMA_64x256{}) : f(BF16_M64{});
+    // M <= 64 with 64-channel multiples: direct-to-LDS 64 x 128 (against register-staged loads,
+    // VGG-19 v2 384 -> 308 us and ResNet-18 l1 109 -> 90 us for the convolution alone, before the
+    // tile went from 64 x 256 to 64 x 128)
+    if (g.M <= 64) return dma ? f(BF16_DMA_64x128{}) : f(BF16_M64{});
     if (dma) {
         // 256 x 256 where M is large and there are enough such tiles
         if (g.M >= 256 && n_tiles(g, 256, 256) >= 192) return f(BF16_DMA_256x256{});

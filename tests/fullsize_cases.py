@@ -25,7 +25,7 @@ CASES = [
     ("alexnet", "conv4", 2, False, 1),    # fp32 64 x 64, channels-last, grouped channel skip
     ("vgg19", "v10", 1, True, 1),         # fp32 128 x 128, 32-deep chunks, with a bias, stream-K
     ("vgg19_bf16", "v1", 1, False, 1),    # bf16 64 x 256, NCHW
-    ("resnet18", "l1.0", 1, False, 1),    # bf16 64 x 256, direct-to-LDS
+    ("resnet18", "l1.0", 1, False, 1),    # bf16 64 x 128, direct-to-LDS
     ("resnet18", "l3.0", 1, False, 1),    # bf16 128 x 128, direct-to-LDS
     ("vgg19_bf16", "v10", 1, False, 1),   # bf16 256 x 256, direct-to-LDS
     ("vgg19_bf16", "v10", 1, True, 1),    # ... with a bias
