@@ -1481,7 +1481,8 @@ template <typename Tr, int WM, int WP, int FM, int FP, int WEAVE> struct Tile {
 // (eight times the fp32 matrix rate per instruction), channels-last layers with
 // 64-channel multiples take direct-to-LDS loads (WEAVE 3): 64 x 128 tiles for
 // M <= 64, 256 x 256 tiles (eight waves of 128 x 64) for M >= 256 where there
-// are enough of them, 128 x 128 elsewhere; the other channels-last layers keep
+// are enough of them, 128 x 64 where 128 x 128 tiles would not fill the compute
+// units, 128 x 128 elsewhere; the other channels-last layers keep
 // two chunks in flight (WEAVE 2), and the rest take 64 x 256, 256 x 256 or
 // 128 x 128 tiles with register-staged loads.
 long long n_tiles(const Geom &g, int tm, int tp) {
@@ -1501,6 +1502,11 @@ using BF16_M64 = Tile<BF16T<32>, 1, 4, 2, 2, 2>;
 using BF16_128x128_K64 = Tile<BF16T<64>, 2, 2, 2, 2, 2>;
 using BF16_256x256 = Tile<BF16T<32>, 2, 2, 4, 4, 2>;
 using BF16_DMA_128x128 = Tile<BF16T<64>, 2, 2, 2, 2, 3>;
+// four waves of 64 x 32, a 48 KB ring (three workgroups a compute unit): for layers with fewer
+// 128 x 128 tiles than compute units (VGG-19 v13-v16 and ResNet-18 layer4, 196 tiles: 63.5 -> 55.5
+// us a layer unprotected); where it only adds a partly filled round it is slower (ResNet-18 l3
+// 49 -> 62 us, l2 62 -> 65 us)
+using BF16_DMA_128x64 = Tile<BF16T<64>, 2, 2, 2, 1, 3>;
 // M <= 64: four waves of 64 x 32, a 48 KB ring, three workgroups a compute unit (against 64 x 256
 // tiles of four 64 x 64 waves, two a compute unit: ResNet-18 l1 89 -> 79 us, VGG-19 v2 299 -> 287 us
 // with the channels-last copy; 64 x 64 tiles of two waves, 64 x 128 of two waves and deeper rings
@@ -1567,6 +1573,7 @@ auto with_tile(const Geom &g, bool nhwc, Fn &&f) {
     if (dma) {
         // 256 x 256 where M is large and there are enough such tiles
         if (g.M >= 256 && n_tiles(g, 256, 256) >= 192) return f(BF16_DMA_256x256{});
+        if (n_tiles(g, 128, 128) < 256) return f(BF16_DMA_128x64{});
         return f(BF16_DMA_128x128{});
     }
     if (g.M >= 256 && n_tiles(g, 256, 256) >= 192) return f(BF16_256x256{});

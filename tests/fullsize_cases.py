@@ -27,6 +27,7 @@ CASES = [
     ("vgg19_bf16", "v1", 1, False, 1),    # bf16 64 x 256, NCHW
     ("resnet18", "l1.0", 1, False, 1),    # bf16 64 x 128, direct-to-LDS
     ("resnet18", "l3.0", 1, False, 1),    # bf16 128 x 128, direct-to-LDS
+    ("resnet18", "l4.0", 1, False, 1),    # bf16 128 x 64, direct-to-LDS (fewer 128 x 128 tiles than CUs)
     ("vgg19_bf16", "v10", 1, False, 1),   # bf16 256 x 256, direct-to-LDS
     ("vgg19_bf16", "v10", 1, True, 1),    # ... with a bias
     # path 0: ftcnn_conv_fwd on the layers whose kernel differs from path 1's
